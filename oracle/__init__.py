@@ -1,0 +1,27 @@
+"""CPU oracle for the SimSD verification step -- TEST INFRASTRUCTURE ONLY.
+
+A plain, slow, float64 numpy statement of what the GPU path computes:
+
+  * ``mask``      slot labels and the token-level temporal attention mask of
+                  Sec. 3.1 (eq. 1), with the prompt visible to every response row
+                  and padding rows/columns removed;
+  * ``attention`` softmax attention of every new row over [cached prefix | new
+                  slots] under that mask (Sec. 3.2, "Target Model Verification");
+  * ``accept``    the greedy (temperature-0) form of the acceptance rule of
+                  eq. 2: argmax with lowest-index ties, softmax confidence, the
+                  target probability of each draft and the accepted prefix length.
+
+Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product path (the C-ABI library and its Python
+binding) never imports, links or calls it, and shares no code with it.  Inputs
+come from the ``synth`` generator; bfloat16 tensors arrive as uint16 bit
+patterns and are widened exactly to float64 here.
+"""
+
+from .widen import widen
+from .mask import slot_labels, new_slot_visibility, DATA, MASK
+from .attention import attend, verify_attention
+from .accept import verify_accept
+
+__all__ = ["widen", "slot_labels", "new_slot_visibility", "DATA", "MASK", "attend",
+           "verify_attention", "verify_accept"]

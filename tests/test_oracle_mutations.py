@@ -1,0 +1,118 @@
+"""The pins must bite: plant a plausible mistake in the oracle (on the CPU, via
+monkeypatching) and check that the golden masks or the brute force reject it."""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import mask as omask, attention as oattn, accept as oacc
+from brute import brute_attention
+from synth import generate
+from test_oracle_mask import small_cfg, read_golden
+import test_oracle_accept as tacc
+
+MASK, DATA = omask.MASK, omask.DATA
+
+
+def golden_ok():
+    for name in ("mask_B3_mu231.txt", "mask_B5_mixed.txt"):
+        rows, meta = read_golden(name)
+        B, L, gamma = meta["block_size"][0], meta["max_ref"][0], meta["num_ref"][0]
+        order = [f"M{k}" for k in range(B)] + [f"D{r + 1}" for r in range(L)]
+        want = np.array([rows[k] for k in order], bool)
+        got = omask.new_slot_visibility(np.array(meta["step_map"]), gamma, L)
+        if not np.array_equal(got, want):
+            return False
+    return True
+
+
+def brute_ok(seeds=(1, 2, 3)):
+    for seed in seeds:
+        cfg = small_cfg(batch=2, block_size=5, max_ref=4, prefix=(0, 6),
+                        num_q_heads=4, num_kv_heads=2, head_dim=8)
+        inp = generate(cfg, seed=seed, poison=True)
+        out, lse = oracle.verify_attention(inp)
+        bo, bl = brute_attention(inp)
+        if not (np.allclose(out, bo, atol=1e-12, rtol=0) and
+                np.allclose(lse, bl, atol=1e-12, rtol=0)):
+            return False
+    return True
+
+
+def _vis_variant(which):
+    def vis(si, ti, sj, tj):
+        if sj == MASK and tj == 0 and which != "committed_hidden":
+            return True
+        if si == DATA and sj == DATA:
+            return tj < ti if which == "case1_strict" else tj <= ti
+        if si == DATA and sj == MASK:
+            return tj >= ti if which == "case2_loose" else tj > ti
+        if si == MASK and sj == DATA:
+            return tj <= ti if which == "case3_loose" else tj < ti
+        return tj > ti if which == "case4_strict" else tj >= ti
+    return vis
+
+
+@pytest.mark.parametrize("which", ["case1_strict", "case2_loose", "case3_loose",
+                                   "case4_strict", "committed_hidden"])
+def test_mask_mutation_caught(monkeypatch, which):
+    assert golden_ok() and brute_ok()
+    monkeypatch.setattr(omask, "visible", _vis_variant(which))
+    assert not (golden_ok() and brute_ok())
+
+
+def test_transposed_mask_caught(monkeypatch):
+    real = omask.new_slot_visibility
+    monkeypatch.setattr(oattn, "new_slot_visibility", lambda *a: real(*a).T.copy())
+    assert not brute_ok()
+
+
+def test_gqa_map_mutation_caught(monkeypatch):
+    """Query head h must use KV head h // G, not h % Hkv."""
+    real = oattn.pair_attention
+
+    def wrong(inp, b, kvh, scale=None):
+        cfg = inp.cfg
+        G, Hkv = cfg.group, cfg.num_kv_heads
+        out = np.zeros((cfg.n_new, G, cfg.head_dim))
+        lse = np.zeros((G, cfg.n_new))
+        for g in range(G):
+            h = kvh * G + g
+            o, l = real(inp, b, h % Hkv, scale)
+            out[:, g], lse[g] = o[:, h % G], l[h % G]
+        return out, lse
+    monkeypatch.setattr(oattn, "pair_attention", wrong)
+    assert not brute_ok()
+
+
+def test_dropped_scale_caught(monkeypatch):
+    real = oattn.attend
+    monkeypatch.setattr(oattn, "attend", lambda q, k, v, vis, scale: real(q, k, v, vis, 1.0))
+    assert not brute_ok()
+
+
+def test_hidden_prefix_caught(monkeypatch):
+    monkeypatch.setattr(oattn, "row_valid", lambda *a: np.zeros(len(a[0]) + a[2], bool))
+    assert not brute_ok()
+
+
+def test_accept_mutations_caught(monkeypatch):
+    """Highest-index ties, or a missing max shift in the log-sum-exp, fail the
+    accept pins."""
+    assert tacc.all_pins_pass()
+
+    def last_tie(x):
+        m = x.max()
+        t = int(np.flatnonzero(x == m)[-1])
+        return t, m, m + math.log(np.exp(x - m).sum())
+    monkeypatch.setattr(oacc, "scan_row", last_tie)
+    assert not tacc.all_pins_pass()
+    monkeypatch.undo()
+
+    def no_log(x):
+        m = x.max()
+        return int(np.flatnonzero(x == m)[0]), m, m + np.exp(x - m).sum()
+    monkeypatch.setattr(oacc, "scan_row", no_log)
+    assert not tacc.all_pins_pass()
