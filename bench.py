@@ -1,0 +1,321 @@
+#!/usr/bin/env python3
+"""Benchmark of the SimSD verification step on one MI355X.
+
+One step = simsd_verify_attention + simsd_verify_accept over one batch of
+seeded synthetic inputs already resident in HBM, launched back to back on one
+stream.  Prints ONE JSON line: verified tokens/s (sum over sequences of the
+drafted tokens checked per step, divided by the step time), the roofline of the
+dominant kernel (attention) measured with HIP events inside the timed region,
+and the CPU oracle's rate on a bounded sample of the same workload.
+
+Inputs are cycled through several copies when one step's bytes fit in the
+256 MB last-level cache, so every step reads its inputs from HBM.
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "verify-step tokens/sec + achieved HBM GB/s (% roofline), 1×MI355X"
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+ATTN_SOURCES = ["paper_2606_02544_amd/csrc/simsd_attention.hip"]
+
+
+def workload_numbers(inp):
+    """Algorithmic bytes and flops of one step (see the design notes)."""
+    cfg = inp.cfg
+    s = cfg.elem_bytes
+    b, Hq, Hkv, d, n_new, B = (cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
+                               cfg.n_new, cfg.block_size)
+    prefix = int(np.sum(inp.prefix_lens.astype(np.int64)))
+    kv_bytes = 2 * prefix * Hkv * d * s
+    new_bytes = b * n_new * (2 * Hq * d * s + 2 * Hkv * d * s) + b * Hq * n_new * 4
+    attn_bytes = kv_bytes + new_bytes
+    scanned = int(np.sum(inp.step_map >= 1))
+    accept_bytes = scanned * cfg.vocab * s
+    # every non-padded row sees prefix + (non-padded block slots) keys; QK^T and PV
+    keys = 0
+    for q in range(b):
+        nonpad = int(np.sum(inp.step_map[q] >= 0))
+        rows = nonpad + int(inp.num_ref[q])
+        keys += rows * (int(inp.prefix_lens[q]) + nonpad)
+    attn_flops = 4 * keys * Hq * d
+    return dict(attn_bytes=attn_bytes, accept_bytes=accept_bytes, attn_flops=attn_flops,
+                verified=int(np.sum(inp.num_ref)))
+
+
+def source_digest(paths):
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"attention_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and line.startswith("- "):
+                k, v = line[2:].split(":", 1)
+                fields[k.strip()] = v.strip().strip("`")
+    if fields.get("source_sha256_16") != source_digest(ATTN_SOURCES):
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(inp, seconds: float):
+    """The oracle (float64 numpy) on the same workload, repeated whole steps
+    until ``seconds`` have passed, or on a subset of (sequence, KV head) pairs
+    plus their sequences' accept rows when one step takes longer."""
+    import oracle
+    from threadpoolctl import threadpool_info
+    cfg = inp.cfg
+    pairs = [(s, h) for s in range(cfg.batch) for h in range(cfg.num_kv_heads)]
+    t0 = time.perf_counter()
+    steps = 0
+    done_pairs = 0
+    tokens = 0.0
+    per_pair_tokens = float(np.sum(inp.num_ref)) / len(pairs)
+    # one step: attention over all pairs, then the accept scan
+    while time.perf_counter() - t0 < seconds:
+        for (s, h) in pairs:
+            oracle.verify_attention(inp, pairs=[(s, h)])
+            done_pairs += 1
+            tokens += per_pair_tokens
+            if time.perf_counter() - t0 >= seconds:
+                break
+        else:
+            oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, cfg.dtype)
+            steps += 1
+    dt = time.perf_counter() - t0
+    if steps == 0:
+        # Partial step: charge the accept scan of the sampled sequences too.
+        seqs = sorted({s for s, _ in pairs[:done_pairs]})
+        t1 = time.perf_counter()
+        sl = np.array(seqs)
+        oracle.verify_accept(inp.logits[sl], inp.draft_ids[sl], inp.step_map[sl],
+                             inp.num_ref[sl], cfg.dtype)
+        dt += time.perf_counter() - t1
+        sample = f"{done_pairs} of {len(pairs)} (sequence, KV head) pairs + accept of {len(seqs)} sequences"
+    else:
+        sample = f"{steps} whole steps" + (f" + {done_pairs - steps * len(pairs)} pairs" if done_pairs > steps * len(pairs) else "")
+    threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
+    return {"value": tokens / dt, "unit": "verified tokens/s", "cores": threads,
+            "kind": "oracle", "sample": sample + f", {dt:.1f} s float64 numpy"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=30)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="workload (1 tiny-f32, 2 sdar-1.7b-layer, 3 sdar-8b-layer, "
+                         "4 long-context, 5 ragged-paged)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--rotate-mb", type=float, default=640.0,
+                    help="cycle input copies until this many MB are touched per cycle")
+    ap.add_argument("--kv-chunk", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
+              "(the verification step shards by sequence / KV head with no exchange; "
+              "see the design notes).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_02544_amd import binding
+    from synth import CONFIGS, generate
+
+    cfg = CONFIGS[args.config]
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
+    inp = generate(cfg)
+    wl = workload_numbers(inp)
+    step_bytes = wl["attn_bytes"] + wl["accept_bytes"]
+    copies = max(1, math.ceil(args.rotate_mb * 1e6 / step_bytes))
+    copies = min(copies, max(1, int(40e9 // step_bytes)))
+
+    def to_dev(a, dt):
+        if dt == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        if dt == "f32":
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(dev)
+
+    dt = cfg.dtype
+    base = dict(q=to_dev(inp.q, dt), k_new=to_dev(inp.k_new, dt), v_new=to_dev(inp.v_new, dt),
+                k_cache=to_dev(inp.k_cache, dt), v_cache=to_dev(inp.v_cache, dt),
+                block_table=None if inp.block_table is None else to_dev(inp.block_table, "i32"),
+                prefix_lens=to_dev(inp.prefix_lens, "i32"), step_map=to_dev(inp.step_map, "i32"),
+                num_ref=to_dev(inp.num_ref, "i32"), logits=to_dev(inp.logits, dt),
+                draft_ids=to_dev(inp.draft_ids, "i32"))
+    sets = [base] + [{k: (None if v is None else v.clone()) for k, v in base.items()}
+                     for _ in range(copies - 1)]
+
+    b, B, L = cfg.batch, cfg.block_size, cfg.max_ref
+    out = torch.empty_like(base["q"])
+    lse = torch.empty((b, cfg.num_q_heads, cfg.n_new), dtype=torch.float32, device=dev)
+    tid = torch.empty((b, B), dtype=torch.int32, device=dev)
+    conf = torch.empty((b, B), dtype=torch.float32, device=dev)
+    dprob = torch.empty((b, L), dtype=torch.float32, device=dev)
+    alen = torch.empty((b,), dtype=torch.int32, device=dev)
+    adesc = binding.attention_desc(
+        base["q"], base["k_cache"], num_kv_heads=cfg.num_kv_heads, block_size=B, max_ref=L,
+        max_prefix_len=cfg.max_prefix, page_size=cfg.page_size,
+        max_pages_per_seq=0 if inp.block_table is None else inp.block_table.shape[1],
+        kv_chunk=args.kv_chunk)
+    cdesc = binding.accept_desc(base["logits"], L)
+    aws_n = binding.attention_workspace_size(adesc)
+    cws_n = binding.accept_workspace_size(cdesc)
+    aws = torch.zeros(max(aws_n, 16), dtype=torch.uint8, device=dev)
+    cws = torch.zeros(max(cws_n, 16), dtype=torch.uint8, device=dev)
+
+    lib = binding.lib()
+    P = ctypes.c_void_p
+    stream = torch.cuda.current_stream()
+    sp = P(stream.cuda_stream)
+    ptr = lambda t: None if t is None else P(t.data_ptr())
+    calls = []
+    for s in sets:
+        a_args = (ctypes.byref(adesc), ptr(s["q"]), ptr(s["k_new"]), ptr(s["v_new"]),
+                  ptr(s["k_cache"]), ptr(s["v_cache"]), ptr(s["block_table"]),
+                  ptr(s["prefix_lens"]), ptr(s["step_map"]), ptr(s["num_ref"]), ptr(out),
+                  ptr(lse), ptr(aws), aws_n, sp)
+        c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]), ptr(s["step_map"]),
+                  ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob), ptr(alen), ptr(cws),
+                  cws_n, sp)
+        calls.append((a_args, c_args))
+    f_attn, f_acc = lib.simsd_verify_attention, lib.simsd_verify_accept
+
+    def step(i):
+        a_args, c_args = calls[i % len(calls)]
+        st = f_attn(*a_args)
+        st |= f_acc(*c_args)
+        return st
+
+    print(f"[bench] {cfg.name}: {copies} input copies, {step_bytes / 1e6:.1f} MB per step; "
+          f"warmup {args.warmup}", file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        if step(i):
+            raise RuntimeError(lib.simsd_last_error().decode())
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    print(f"[bench] timing {K} steps", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        e0, e1, e2 = ev[i]
+        a_args, c_args = calls[i % len(calls)]
+        e0.record(stream)
+        f_attn(*a_args)
+        e1.record(stream)
+        f_acc(*c_args)
+        e2.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    attn_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    acc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    print(f"[bench] done: {elapsed / K * 1e3:.4f} ms/step (attention {attn_ms * 1e3:.2f} us, "
+          f"accept {acc_ms * 1e3:.2f} us)", file=sys.stderr, flush=True)
+
+    parity = None
+    if not args.no_check:
+        import oracle
+        o = out.float().cpu().double().numpy()
+        l_ = lse.cpu().double().numpy()
+        pairs = [(0, 0), (b - 1, cfg.num_kv_heads - 1)]
+        ro, rl = oracle.verify_attention(inp, pairs=pairs)
+        G = cfg.group
+        ok = True
+        for s_, h_ in pairs:
+            sl = slice(h_ * G, (h_ + 1) * G)
+            err = np.abs(o[s_, :, sl] - ro[s_, :, sl]).max(-1)
+            ref = np.abs(ro[s_, :, sl]).max(-1)
+            tol = 2e-2 * ref if dt == "bf16" else np.full_like(ref, 1e-5)
+            ok &= bool(np.all(err <= tol))
+            ok &= bool(np.all(np.abs(l_[s_, sl] - rl[s_, sl]) <= 1e-4 * np.maximum(1, np.abs(rl[s_, sl]))))
+        rt, _, _, ra = oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, dt)
+        ok &= bool(np.array_equal(tid.cpu().numpy(), rt)) and bool(np.array_equal(alen.cpu().numpy(), ra))
+        parity = {"checked": f"attention pairs {pairs}, accept all rows", "ok": ok}
+
+    value = wl["verified"] * K / elapsed
+    attn_gbs = wl["attn_bytes"] / (attn_ms * 1e-3) / 1e9
+    traffic = recorded_traffic(cfg.name)
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "verified tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / K * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if dt == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: batch {b}, {cfg.num_q_heads}/{cfg.num_kv_heads} heads, "
+                        f"head_dim {cfg.head_dim}, prefix {cfg.prefix}, block {B}, "
+                        f"{L} reference slots, vocab {cfg.vocab}"
+                        + (f", paged {cfg.page_size}" if cfg.page_size else ""),
+            "step_hbm_bytes": step_bytes,
+            "step_hbm_gbs": step_bytes / (elapsed / K) / 1e9,
+            "step_roofline_frac": step_bytes / (elapsed / K) / 1e9 / HBM_PEAK_GBS,
+            "attention_us": attn_ms * 1e3,
+            "accept_us": acc_ms * 1e3,
+            "accept_gbs": wl["accept_bytes"] / (acc_ms * 1e-3) / 1e9,
+            "attention_mfma_frac": wl["attn_flops"] / (attn_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+            "input_copies": copies,
+            "hip_graph": False,
+            "kv_chunk": args.kv_chunk,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": attn_gbs,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": attn_gbs / HBM_PEAK_GBS,
+            "traffic": traffic,
+        },
+        "parity": parity,
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

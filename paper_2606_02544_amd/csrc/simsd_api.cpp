@@ -1,0 +1,110 @@
+// extern "C" compute entry points: check, plan, fill the argument block, launch.
+#include <hip/hip_runtime.h>
+
+#include <string>
+
+#include "simsd.h"
+#include "simsd_kernels.h"
+#include "simsd_plan.h"
+
+using namespace simsd;
+
+static simsd_status hip_fail(hipError_t e, const char* what) {
+  set_error(std::string(what) + ": " + hipGetErrorString(e));
+  return SIMSD_ERR_HIP;
+}
+
+extern "C" simsd_status simsd_verify_attention(
+    const simsd_attn_desc* desc, const void* q, const void* k_new, const void* v_new,
+    const void* k_cache, const void* v_cache, const int32_t* block_table,
+    const int32_t* prefix_lens, const int32_t* step_map, const int32_t* num_ref, void* out,
+    float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    AttnPlan p;
+    simsd_status st = plan_attention(desc, &p);
+    if (st != SIMSD_OK) return st;
+    st = check_attention_args(desc, p, q, k_new, v_new, k_cache, v_cache, block_table,
+                              prefix_lens, step_map, num_ref, out, lse, workspace,
+                              workspace_bytes);
+    if (st != SIMSD_OK) return st;
+    AttnArgs a{};
+    a.q = q;
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.k_cache = k_cache;
+    a.v_cache = v_cache;
+    a.block_table = desc->page_size > 0 ? block_table : nullptr;
+    a.prefix_lens = prefix_lens;
+    a.step_map = step_map;
+    a.num_ref = num_ref;
+    a.out = out;
+    a.lse = lse;
+    a.tickets = p.workspace ? static_cast<int32_t*>(workspace) : nullptr;
+    a.part = p.workspace
+                 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + p.ticket_bytes)
+                 : nullptr;
+    a.cs_seq = desc->cache_stride_seq;
+    a.cs_tok = desc->cache_stride_token;
+    a.cs_head = desc->cache_stride_head;
+    a.hq = desc->num_q_heads;
+    a.hkv = desc->num_kv_heads;
+    a.group = p.group;
+    a.B = desc->block_size;
+    a.L = desc->max_ref;
+    a.n_new = p.n_new;
+    a.rows = p.rows;
+    a.rows_pb = p.rows_pb;
+    a.row_blocks = p.row_blocks;
+    a.page_size = desc->page_size > 0 ? desc->page_size : 1;
+    a.max_pages = desc->max_pages_per_seq;
+    a.chunk = p.chunk;
+    a.splits = p.splits;
+    a.max_prefix = desc->max_prefix_len;
+    a.scale_log2 = p.scale_log2;
+    const hipError_t e = launch_attention(*desc, p, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "simsd_verify_attention launch");
+    return SIMSD_OK;
+  } catch (...) {
+    set_error("simsd_verify_attention: internal error");
+    return SIMSD_ERR_HIP;
+  }
+}
+
+extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const void* logits,
+                                            const int32_t* draft_ids, const int32_t* step_map,
+                                            const int32_t* num_ref, int32_t* target_ids,
+                                            float* confidence, float* draft_prob,
+                                            int32_t* accept_len, void* workspace,
+                                            size_t workspace_bytes, void* stream) {
+  try {
+    AcceptPlan p;
+    simsd_status st = plan_accept(desc, &p);
+    if (st != SIMSD_OK) return st;
+    st = check_accept_args(desc, p, logits, draft_ids, step_map, num_ref, target_ids,
+                           confidence, draft_prob, accept_len, workspace, workspace_bytes);
+    if (st != SIMSD_OK) return st;
+    AcceptArgs a{};
+    a.logits = logits;
+    a.draft_ids = draft_ids;
+    a.step_map = step_map;
+    a.num_ref = num_ref;
+    a.target_ids = target_ids;
+    a.confidence = confidence;
+    a.draft_prob = draft_prob;
+    a.accept_len = accept_len;
+    a.tickets = static_cast<int32_t*>(workspace);
+    a.part = reinterpret_cast<AcceptPartial*>(static_cast<char*>(workspace) + p.ticket_bytes);
+    a.nvec = p.nvec;
+    a.chunk_vecs = p.chunk_vecs;
+    a.B = desc->block_size;
+    a.L = desc->max_ref;
+    a.V = desc->vocab;
+    a.cpr = p.cpr;
+    const hipError_t e = launch_accept(*desc, p, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept launch");
+    return SIMSD_OK;
+  } catch (...) {
+    set_error("simsd_verify_accept: internal error");
+    return SIMSD_ERR_HIP;
+  }
+}

@@ -1,0 +1,52 @@
+// Device-side argument blocks and launch entry points of the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "simsd_plan.h"
+
+namespace simsd {
+
+struct AttnArgs {
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* block_table;
+  const int32_t* prefix_lens;
+  const int32_t* step_map;
+  const int32_t* num_ref;
+  void* out;
+  float* lse;
+  float* part;        // split partials (workspace), or null when splits == 1
+  int32_t* tickets;   // one completion counter per (sequence, KV head, row block)
+  int64_t cs_seq, cs_tok, cs_head;
+  int hq, hkv, group, B, L, n_new, rows, rows_pb, row_blocks;
+  int page_size, max_pages, chunk, splits, max_prefix;
+  float scale_log2;
+};
+
+struct AcceptArgs {
+  const void* logits;
+  const int32_t* draft_ids;
+  const int32_t* step_map;
+  const int32_t* num_ref;
+  int32_t* target_ids;
+  float* confidence;
+  float* draft_prob;
+  int32_t* accept_len;
+  AcceptPartial* part;
+  int32_t* tickets;
+  int64_t nvec, chunk_vecs;
+  int B, L, V, cpr;
+};
+
+hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const AttnArgs& a,
+                            hipStream_t stream);
+hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const AcceptArgs& a,
+                         hipStream_t stream);
+
+}  // namespace simsd

@@ -1,0 +1,73 @@
+// Launch planning and argument checking for the SimSD verification step.
+// Pure host C++ (no HIP): every decision here is testable without a GPU.
+#pragma once
+
+#include <cstddef>
+#include <cstdint>
+#include <string>
+
+#include "simsd.h"
+
+namespace simsd {
+
+constexpr int kTile = 64;            // keys per attention tile
+constexpr int kMaxNew = 64;          // B + L limit (one 64-bit visibility word per row)
+constexpr int kMaxGroup = 16;        // Hq / Hkv limit
+constexpr int kTargetUnits = 512;    // work-groups the split heuristic aims for (2 per CU)
+constexpr int kMaxAutoChunk = 4096;  // longest automatic prefix chunk (keys)
+constexpr int kAcceptThreads = 256;  // threads of the vocabulary-scan work-group
+constexpr int kAcceptTarget = 2048;  // scan work-groups the chunk heuristic aims for
+
+struct AttnPlan {
+  int group = 0;        // Hq / Hkv
+  int n_new = 0;        // B + L
+  int rows = 0;         // M = group * n_new packed query rows per (sequence, KV head)
+  int waves = 0;        // waves per work-group
+  int rows_pb = 0;      // rows per work-group (row block)
+  int row_blocks = 0;   // ceil(rows / rows_pb)
+  int chunk = 0;        // prefix keys per split
+  int splits = 0;       // grid.x: ceil(max_prefix_len / chunk), >= 1
+  int64_t pairs = 0;    // batch * Hkv * row_blocks (one ticket each)
+  size_t part_floats = 0;   // floats per split partial: rows_pb * (head_dim + 2)
+  size_t ticket_bytes = 0;  // bytes reserved for tickets at the start of the workspace
+  size_t workspace = 0;     // total bytes
+  float scale_log2 = 0.f;   // softmax scale * log2(e)
+};
+
+struct AcceptPlan {
+  int vec = 1;            // elements per vector load (16 bytes), or 1 for the scalar path
+  int64_t nvec = 0;       // vectors per row
+  int cpr = 0;            // chunks (work-groups) per row
+  int64_t chunk_vecs = 0; // vectors per chunk
+  size_t ticket_bytes = 0;
+  size_t workspace = 0;
+};
+
+// Partial result of one vocabulary chunk: max, lowest index reaching it,
+// sum of exp(x - max).
+struct AcceptPartial {
+  float mx;
+  int32_t ix;
+  float sm;
+  int32_t pad;
+};
+
+void set_error(const std::string& msg);
+
+simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p);
+simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, const void* q,
+                                  const void* k_new, const void* v_new, const void* k_cache,
+                                  const void* v_cache, const int32_t* block_table,
+                                  const int32_t* prefix_lens, const int32_t* step_map,
+                                  const int32_t* num_ref, const void* out, const float* lse,
+                                  const void* workspace, size_t workspace_bytes);
+
+simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p);
+simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
+                               const void* logits, const int32_t* draft_ids,
+                               const int32_t* step_map, const int32_t* num_ref,
+                               const int32_t* target_ids, const float* confidence,
+                               const float* draft_prob, const int32_t* accept_len,
+                               const void* workspace, size_t workspace_bytes);
+
+}  // namespace simsd

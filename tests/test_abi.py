@@ -1,0 +1,166 @@
+"""The C ABI on the CPU: the library loads, exports every declared symbol,
+sizes workspaces, and rejects bad arguments before any device work.
+
+Every compute call made here fails host validation, so no kernel is ever
+launched (pointer values are small aligned fakes that are never dereferenced)."""
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_02544_amd import binding
+from paper_2606_02544_amd.binding import AttnDesc, AcceptDesc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "simsd.h")
+
+FAKE = ctypes.c_void_p(0x10000)     # aligned, never dereferenced
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(simsd_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = binding.lib()
+    names = declared_functions()
+    assert len(names) >= 8
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.simsd_version() == 100
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", "/nonexistent/libsimsd.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        binding.lib()
+
+
+def cfg_desc(cid, **kw):
+    from synth import CONFIGS
+    c = CONFIGS[cid]
+    d = c.head_dim
+    if c.page_size:
+        strides = (c.page_size * c.num_kv_heads * d, c.num_kv_heads * d, d)
+        pages = -(-c.max_prefix // c.page_size)
+    else:
+        strides = (c.max_prefix * c.num_kv_heads * d, c.num_kv_heads * d, d)
+        pages = 0
+    base = dict(batch=c.batch, num_q_heads=c.num_q_heads, num_kv_heads=c.num_kv_heads,
+                head_dim=d, block_size=c.block_size, max_ref=c.max_ref,
+                max_prefix_len=c.max_prefix, page_size=c.page_size, max_pages_per_seq=pages,
+                kv_chunk=0, cache_stride_seq=strides[0], cache_stride_token=strides[1],
+                cache_stride_head=strides[2], scale=0.0,
+                dtype=binding.SIMSD_F32 if c.dtype == "f32" else binding.SIMSD_BF16)
+    base.update(kw)
+    return AttnDesc(**base)
+
+
+def test_workspace_sizes_follow_the_plan():
+    # config 4: 16 x 8 pairs, 256 packed rows, chunk 4096 -> 4 splits;
+    # 256-byte ticket block + 128 * 4 partials of 256 rows x (128 + 2) floats.
+    assert binding.attention_workspace_size(cfg_desc(4)) == 512 + 128 * 4 * 256 * 130 * 4
+    # a single split needs no workspace
+    assert binding.attention_workspace_size(cfg_desc(1, kv_chunk=64)) == 0
+    assert binding.attention_workspace_size(cfg_desc(2)) > 0
+    assert binding.attention_workspace_size(cfg_desc(1, head_dim=96)) == 0   # invalid -> 0
+    acc = AcceptDesc(batch=16, block_size=32, max_ref=32, vocab=151936, chunks_per_row=0,
+                     logits_dtype=binding.SIMSD_BF16)
+    # 512 rows -> 4 chunks per row; 256-byte tickets + 16-byte partials
+    assert binding.accept_workspace_size(acc) == 256 + 512 * 4 * 16
+
+
+def call_attention(desc, **over):
+    args = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_cache=FAKE, v_cache=FAKE, block_table=FAKE,
+                prefix_lens=FAKE, step_map=FAKE, num_ref=FAKE, out=FAKE, lse=None,
+                workspace=None, ws_bytes=0)
+    args.update(over)
+    lib = binding.lib()
+    st = lib.simsd_verify_attention(ctypes.byref(desc), args["q"], args["k_new"], args["v_new"],
+                                    args["k_cache"], args["v_cache"], args["block_table"],
+                                    args["prefix_lens"], args["step_map"], args["num_ref"],
+                                    args["out"], args["lse"], args["workspace"],
+                                    args["ws_bytes"], None)
+    return st, lib.simsd_last_error().decode()
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("head_dim", 96, 3), ("head_dim", 256, 3), ("num_q_heads", 6, 2), ("num_kv_heads", 0, 2),
+    ("num_q_heads", 136, 3), ("block_size", 0, 2), ("max_ref", 5, 2), ("block_size", 40, 2),
+    ("batch", 0, 2), ("batch", 70000, 2), ("max_prefix_len", -1, 2), ("kv_chunk", 100, 2),
+    ("kv_chunk", -64, 2), ("page_size", -2, 2), ("cache_stride_token", 12, 4),
+    ("cache_stride_head", -8, 2), ("scale", -1.0, 2), ("scale", float("inf"), 2),
+    ("dtype", 7, 3),
+])
+def test_attention_descriptor_errors(field, value, status):
+    desc = cfg_desc(2)
+    if field == "block_size" and value == 40:
+        desc.max_ref = 30                  # B + L = 70 > 64
+    setattr(desc, field, value)
+    st, msg = call_attention(desc, workspace=FAKE, ws_bytes=1 << 40)
+    assert st == status, (st, msg)
+    assert msg
+
+
+def test_attention_pointer_alignment_and_workspace_errors():
+    desc = cfg_desc(2)
+    ws = binding.attention_workspace_size(desc)
+    assert call_attention(desc, q=None, workspace=FAKE, ws_bytes=ws)[0] == 1
+    assert call_attention(desc, k_cache=None, workspace=FAKE, ws_bytes=ws)[0] == 1
+    assert call_attention(desc, out=ctypes.c_void_p(0x10008), workspace=FAKE, ws_bytes=ws)[0] == 4
+    assert call_attention(desc, lse=ctypes.c_void_p(0x10002), workspace=FAKE, ws_bytes=ws)[0] == 4
+    assert call_attention(desc, workspace=None, ws_bytes=0)[0] == 5
+    assert call_attention(desc, workspace=FAKE, ws_bytes=ws - 1)[0] == 5
+    paged = cfg_desc(5)
+    assert call_attention(paged, block_table=None,
+                          workspace=FAKE, ws_bytes=1 << 40)[0] == 1
+    paged.max_pages_per_seq = 3
+    assert call_attention(paged, workspace=FAKE, ws_bytes=1 << 40)[0] == 2
+
+
+def call_accept(desc, **over):
+    a = dict(logits=FAKE, draft_ids=FAKE, step_map=FAKE, num_ref=FAKE, target_ids=FAKE,
+             confidence=None, draft_prob=None, accept_len=FAKE, workspace=FAKE, ws=1 << 30)
+    a.update(over)
+    lib = binding.lib()
+    return lib.simsd_verify_accept(ctypes.byref(desc), a["logits"], a["draft_ids"],
+                                   a["step_map"], a["num_ref"], a["target_ids"],
+                                   a["confidence"], a["draft_prob"], a["accept_len"],
+                                   a["workspace"], a["ws"], None)
+
+
+def test_accept_errors():
+    good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, chunks_per_row=0,
+                logits_dtype=binding.SIMSD_BF16)
+    for k, v, st in [("batch", 0, 2), ("block_size", 65, 2), ("max_ref", 5, 2),
+                     ("vocab", 0, 2), ("chunks_per_row", -1, 2), ("logits_dtype", 3, 3)]:
+        d = AcceptDesc(**dict(good, **{k: v}))
+        assert call_accept(d) == st, k
+    d = AcceptDesc(**good)
+    assert call_accept(d, logits=None) == 1
+    assert call_accept(d, draft_ids=None) == 1
+    assert call_accept(d, logits=ctypes.c_void_p(0x10004)) == 4
+    assert call_accept(d, workspace=None) == 5
+    assert call_accept(d, ws=binding.accept_workspace_size(d) - 1) == 5
+
+
+def test_validate_step_map():
+    ok = np.array([[2, 1, 0, -1, 9], [1, 2, 3, 4, 5]])
+    binding.validate_step_map(ok, [2, 5], max_ref=5)
+    for sm, nr in [([[1, 1, 0, 0, 0]], [2]), ([[2, 3, 0, 0, 0]], [2]), ([[1, 2, 0, 0, 0]], [6]),
+                   ([[1, 0, 0, 0, 0]], [-1])]:
+        with pytest.raises(binding.SimsdError) as e:
+            binding.validate_step_map(np.array(sm), nr, max_ref=5)
+        assert e.value.status == 6
+
+
+def test_status_strings():
+    lib = binding.lib()
+    for code, name in binding.STATUS.items():
+        assert lib.simsd_status_string(code).decode() == name

@@ -1,0 +1,178 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Attention outputs: bf16 within 2e-2 of each row's largest |value|, f32 within
+1e-5 absolute, LSE within 1e-4.  target_ids and accept_len: bit-exact.
+Confidence and draft probabilities: 1e-4 relative.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (DeviceInputs, run_attention, run_accept, check_attention, check_accept,
+                      oracle_accept)
+from synth import CONFIGS, VerifyConfig, generate
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
+    sys.__stderr__.flush()
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+
+
+def _full_parity(inp, kv_chunk=0, chunks_per_row=0):
+    d = DeviceInputs(inp)
+    out, lse = run_attention(d, kv_chunk)
+    ref_out, ref_lse = oracle.verify_attention(inp)
+    check_attention(out, lse, ref_out, ref_lse, inp.cfg.dtype)
+    check_accept(run_accept(d, chunks_per_row), oracle_accept(inp))
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3])
+def test_config_full(cid):
+    inp = generate(CONFIGS[cid], poison=True)
+    _full_parity(inp)
+
+
+@pytest.mark.parametrize("cid", [4, 5])
+def test_config_full_size_sampled(cid):
+    """Full-size workloads in the benchmark's launch configuration; the oracle
+    computes a sample of (sequence, KV head) pairs, the accept step fully."""
+    inp = generate(CONFIGS[cid], poison=True)
+    d = DeviceInputs(inp)
+    out, lse = run_attention(d)
+    lens = inp.prefix_lens
+    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), 0, inp.cfg.batch - 1})
+    pairs = [(s, h) for s in seqs for h in (0, inp.cfg.num_kv_heads - 1)]
+    ref_out, ref_lse = oracle.verify_attention(inp, pairs=pairs)
+    G = inp.cfg.group
+    for s, h in pairs:
+        sl = slice(h * G, (h + 1) * G)
+        check_attention(out[s, :, sl], lse[s, sl], ref_out[s, :, sl], ref_lse[s, sl], "bf16")
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+    check_accept(run_accept(d), oracle_accept(inp))
+
+
+MIXED = [
+    # dtype, head_dim, Hq, Hkv, B, L, prefix, page, kv_chunk, seed
+    ("bf16", 128, 8, 2, 8, 8, (0, 300), 0, 64, 1),
+    ("bf16", 128, 4, 4, 5, 3, (1, 200), 16, 128, 2),
+    ("bf16", 64, 6, 2, 4, 4, (60, 130), 0, 64, 3),
+    ("bf16", 64, 16, 1, 16, 16, (0, 150), 7, 64, 4),
+    ("bf16", 128, 2, 2, 1, 1, (0, 70), 0, 0, 5),
+    ("bf16", 128, 32, 8, 8, 0, (64, 64), 0, 0, 6),
+    ("bf16", 128, 12, 4, 3, 2, (0, 0), 0, 0, 7),
+    ("bf16", 128, 16, 2, 32, 32, (100, 400), 16, 64, 8),
+    ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
+    ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
+    ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
+    ("f32", 64, 16, 2, 16, 16, (30, 150), 0, 0, 12),
+]
+
+
+@pytest.mark.parametrize("case", MIXED, ids=lambda c: "-".join(map(str, c)))
+def test_mixed_step_maps(case):
+    """Per-sequence gamma < B, committed, undrafted and padding slots, ragged
+    prefixes (including empty), paged caches, forced small chunks (several
+    splits and ragged tails), NaN-poisoned cache tails, out-of-range drafts."""
+    dt, d, hq, hkv, B, L, prefix, page, kv_chunk, seed = case
+    cfg = VerifyConfig(0, "mixed", dt, batch=5, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                       prefix=prefix, block_size=B, max_ref=L, vocab=1000 + 8 * seed,
+                       page_size=page, plant=0.6, qkv_std=0.3 if dt == "bf16" else 1.0,
+                       step_mode="mixed")
+    inp = generate(cfg, seed=seed, poison=True, bad_draft_rate=0.3)
+    _full_parity(inp, kv_chunk=kv_chunk, chunks_per_row=0)
+
+
+def test_max_new_slots_and_group():
+    """B + L = 64 new slots and 16 query heads per KV head: 1024 packed rows,
+    several row blocks."""
+    cfg = VerifyConfig(0, "wide", "bf16", batch=2, num_q_heads=32, num_kv_heads=2,
+                       head_dim=128, prefix=(200, 333), block_size=32, max_ref=32,
+                       vocab=4096, qkv_std=0.25, step_mode="mixed")
+    _full_parity(generate(cfg, seed=31, poison=True), kv_chunk=128)
+
+
+def test_split_count_invariance_and_determinism():
+    inp = generate(CONFIGS[3].replace(batch=2, prefix=1000), seed=77, poison=True)
+    d = DeviceInputs(inp)
+    ref_out, ref_lse = oracle.verify_attention(inp)
+    outs = []
+    for chunk in (64, 192, 1024, 0, 0):
+        out, lse = run_attention(d, chunk)
+        check_attention(out, lse, ref_out, ref_lse, "bf16")
+        outs.append((out, lse))
+    np.testing.assert_array_equal(outs[-1][0], outs[-2][0])   # same launch: same bits
+    np.testing.assert_array_equal(outs[-1][1], outs[-2][1])
+    ref = oracle_accept(inp)
+    for cpr in (1, 3, 17, 0):
+        check_accept(run_accept(d, cpr), ref)
+
+
+def test_workspace_reuse_many_launches():
+    """Completion tickets return to zero: repeated launches on one workspace
+    keep producing the same result."""
+    inp = generate(CONFIGS[2], seed=5)
+    d = DeviceInputs(inp)
+    first = run_attention(d, 64)
+    acc0 = run_accept(d, 0)
+    for _ in range(20):
+        out, lse = run_attention(d, 64)
+        np.testing.assert_array_equal(out, first[0])
+        np.testing.assert_array_equal(lse, first[1])
+        acc = run_accept(d, 0)
+        np.testing.assert_array_equal(acc[0], acc0[0])
+        np.testing.assert_array_equal(acc[3], acc0[3])
+
+
+def _accept_case(logits, drafts, step, gamma, dtype, cprs=(0, 1, 2, 5)):
+    from synth import bf16_bits_from_f32
+    x = logits.astype(np.float32)
+    stored = bf16_bits_from_f32(x) if dtype == "bf16" else x
+    ref = oracle.verify_accept(stored, drafts, step, gamma, dtype)
+    from gpu_util import dev_tensor, int_tensor
+    from paper_2606_02544_amd import binding
+    for cpr in cprs:
+        got = binding.verify_accept(dev_tensor(stored, dtype), int_tensor(drafts),
+                                    int_tensor(step), int_tensor(gamma), chunks_per_row=cpr)
+        torch.cuda.synchronize()
+        got = tuple(t.cpu().numpy().astype(np.float64) if t.dtype == torch.float32
+                    else t.cpu().numpy() for t in got)
+        check_accept(got, ref)
+    return ref
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("V", [5, 8, 1003, 4096, 151936])
+def test_accept_ties_zeros_and_bad_drafts(dtype, V):
+    rng = np.random.default_rng(V)
+    b, B, L = 3, 6, 5
+    x = np.round(rng.standard_normal((b, B, V)) * 4) / 4          # many exact ties
+    x[0, 1, :] = -1.0
+    x[0, 1, [V // 3, V - 1]] = 0.0                                # +0 / -0 tie
+    x[0, 1, V - 1] = -0.0
+    x[1, 2, :] = 3.0                                              # constant row
+    x[2, 0, V - 1] = 50.0                                         # max in the last element
+    step = np.array([[2, 1, 3, 4, 5, 0], [1, -1, 2, 0, 6, 3], [1, 2, 3, 4, 5, 6]], np.int32)
+    gamma = np.array([5, 3, 0], np.int32)
+    argmax = lambda s, k: int(np.argmax(x[s, k].astype(np.float32)))
+    drafts = np.full((b, L), -1, np.int32)
+    drafts[0] = [argmax(0, 1), argmax(0, 0), V, argmax(0, 3), -3]
+    drafts[1, :3] = [argmax(1, 0), 0, argmax(1, 5)]
+    ref = _accept_case(x, drafts, step, gamma, dtype)
+    assert ref[3][2] == 0
+
+
+def test_accept_bench_shape_chunking():
+    inp = generate(CONFIGS[2], seed=11)
+    d = DeviceInputs(inp)
+    ref = oracle_accept(inp)
+    for cpr in (1, 7, 64, 0):
+        check_accept(run_accept(d, cpr), ref)
