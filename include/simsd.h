@@ -48,10 +48,10 @@
  *    them is undefined: step maps as above, 0 <= prefix_lens[b] <=
  *    max_prefix_len, block_table ids inside the page pool, finite inputs.
  *  - Workspace: caller-owned device memory of at least the size the matching
- *    *_workspace_size() call returns, ZEROED ONCE by the caller when it is
- *    allocated.  Every launch leaves its completion counters at zero again, so
- *    a workspace can be reused by later launches on the same stream.  Two calls
- *    in flight at the same time need two workspaces.
+ *    *_workspace_size() call returns (it may be 0, and then the pointer may
+ *    be NULL).  It holds per-chunk partial results between the kernels of one
+ *    call; its contents need no initialisation and are meaningless afterwards.
+ *    Two calls in flight at the same time need two workspaces.
  */
 #ifndef SIMSD_H
 #define SIMSD_H
@@ -162,7 +162,7 @@ simsd_status simsd_verify_attention(const simsd_attn_desc* desc, const void* q,
 
 typedef struct {
   int32_t batch;             /* sequences, >= 1                                    */
-  int32_t block_size;        /* B >= 1                                             */
+  int32_t block_size;        /* B, 1 <= B <= 64                                    */
   int32_t max_ref;           /* L, 0 <= L <= B                                     */
   int32_t vocab;             /* V >= 1                                             */
   int32_t chunks_per_row;    /* work-groups per logits row, or 0 = library's choice */

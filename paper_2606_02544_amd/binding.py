@@ -105,10 +105,8 @@ def _stream(stream) -> ctypes.c_void_p:
 
 
 class _Workspaces:
-    """Zero-initialised workspaces, one per (device, kind), grown on demand.
-
-    The kernels return their completion counters to zero, so a workspace is
-    reused by later calls on the same stream without clearing it again."""
+    """Scratch buffers for the workspace argument, one per (device, kind),
+    grown on demand.  The library needs no initialised contents."""
 
     def __init__(self):
         self._bufs = {}
@@ -119,9 +117,12 @@ class _Workspaces:
         key = (str(device), kind)
         buf = self._bufs.get(key)
         if buf is None or buf.numel() < nbytes:
-            buf = torch.zeros(nbytes, dtype=torch.uint8, device=device)
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
             self._bufs[key] = buf
         return buf
+
+    def clear(self):
+        self._bufs.clear()
 
 
 WORKSPACES = _Workspaces()

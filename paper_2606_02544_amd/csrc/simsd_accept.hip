@@ -6,8 +6,8 @@
 // chunks; one work-group streams a chunk with 16-byte loads and keeps, per
 // lane, the running maximum, the first vector reaching it and the sum of
 // exp(x - max).  Partials are merged in (value desc, index asc) order, so ties
-// resolve to the lowest vocabulary index exactly.  The last work-group of a
-// sequence (per-sequence ticket) merges the chunks of all its rows, computes
+// resolve to the lowest vocabulary index exactly.  A second kernel, one
+// work-group per sequence, merges the chunks of all its rows, computes
 // confidence and draft probabilities and walks the drafts in step order.
 #include "simsd_kernels.h"
 
@@ -143,50 +143,50 @@ __device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, Bes
   return r;
 }
 
+// One work-group per (vocabulary chunk, block slot, sequence): writes the
+// chunk's (max, lowest index, sum of exp) to the workspace.
 template <bool BF16, int VEC>
-__global__ void __launch_bounds__(NT) accept_kernel(AcceptArgs a) {
+__global__ void __launch_bounds__(NT) scan_kernel(AcceptArgs a) {
   __shared__ Best s_red[NT / 64];
+  const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
+  const int64_t rowi = static_cast<int64_t>(b) * a.B + k;
+  if (a.step_map[rowi] < 1) return;          // committed or padding: not scanned
+  const int esz = BF16 ? 2 : 4;
+  const char* row = static_cast<const char*>(a.logits) + rowi * a.V * esz;
+  const int64_t v0 = static_cast<int64_t>(c) * a.chunk_vecs;
+  const int64_t v1 = min(a.nvec, v0 + a.chunk_vecs);
+  const Best r = scan_chunk<BF16, VEC>(row, v0, v1, threadIdx.x, s_red);
+  if (threadIdx.x == 0) {
+    AcceptPartial pr;
+    pr.mx = r.mx;
+    pr.ix = r.ix;
+    pr.sm = r.sm;
+    pr.pad = 0;
+    a.part[rowi * a.cpr + c] = pr;
+  }
+}
+
+// One work-group per sequence: merge the chunks of every row, then the
+// per-row outputs, draft probabilities and the accepted-prefix length.
+template <bool BF16>
+__global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
   __shared__ Best s_row[kMaxNew];
   __shared__ int s_row_of_step[kMaxNew];
-  __shared__ int s_last;
-  const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(b) * a.B;
   const int esz = BF16 ? 2 : 4;
   const char* logits_b = static_cast<const char*>(a.logits) + static_cast<int64_t>(b) * a.B * a.V * esz;
-
-  Best res = {kNegInf, kNoIndex, 0.f};
-  if (step_row[k] >= 1) {
-    const int64_t v0 = static_cast<int64_t>(c) * a.chunk_vecs;
-    const int64_t v1 = min(a.nvec, v0 + a.chunk_vecs);
-    res = scan_chunk<BF16, VEC>(logits_b + static_cast<int64_t>(k) * a.V * esz, v0, v1, tid, s_red);
-  }
-  AcceptPartial* part = a.part + (static_cast<int64_t>(b) * a.B + k) * a.cpr;
-  if (tid == 0) {
-    AcceptPartial pr;
-    pr.mx = res.mx;
-    pr.ix = res.ix;
-    pr.sm = res.sm;
-    pr.pad = 0;
-    part[c] = pr;
-  }
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(a.tickets + b, 1) == a.B * a.cpr - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
-  // Last work-group of sequence b: merge every row.
-  const int lane = tid & 63, wave = tid >> 6;
   const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.B * a.cpr;
   for (int kk = wave; kk < a.B; kk += NT / 64) {
     Best r = {kNegInf, kNoIndex, 0.f};
-    for (int cc = lane; cc < a.cpr; cc += 64) {
-      const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
-      r = combine(r, Best{pr.mx, pr.ix, pr.sm});
+    if (step_row[kk] >= 1) {
+      for (int cc = lane; cc < a.cpr; cc += 64) {
+        const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
+        r = combine(r, Best{pr.mx, pr.ix, pr.sm});
+      }
+      r = wave_reduce(r);
     }
-    r = wave_reduce(r);
     if (lane == 0) s_row[kk] = r;
   }
   const int gamma = min(max(a.num_ref[b], 0), a.L);
@@ -219,7 +219,6 @@ __global__ void __launch_bounds__(NT) accept_kernel(AcceptArgs a) {
       ++acc;
     }
     a.accept_len[b] = acc;
-    atomicExch(a.tickets + b, 0);
   }
 }
 
@@ -229,13 +228,18 @@ hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const 
                          hipStream_t st) {
   const dim3 grid(p.cpr, d.block_size, d.batch);
   const dim3 block(NT);
-  if (d.logits_dtype == SIMSD_BF16) {
-    if (p.vec == 8) hipLaunchKernelGGL((accept_kernel<true, 8>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((accept_kernel<true, 1>), grid, block, 0, st, a);
+  const bool bf16 = d.logits_dtype == SIMSD_BF16;
+  if (bf16) {
+    if (p.vec == 8) hipLaunchKernelGGL((scan_kernel<true, 8>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<true, 1>), grid, block, 0, st, a);
   } else {
-    if (p.vec == 4) hipLaunchKernelGGL((accept_kernel<false, 4>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((accept_kernel<false, 1>), grid, block, 0, st, a);
+    if (p.vec == 4) hipLaunchKernelGGL((scan_kernel<false, 4>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<false, 1>), grid, block, 0, st, a);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (bf16) hipLaunchKernelGGL((finalize_kernel<true>), dim3(d.batch), block, 0, st, a);
+  else hipLaunchKernelGGL((finalize_kernel<false>), dim3(d.batch), block, 0, st, a);
   return hipGetLastError();
 }
 

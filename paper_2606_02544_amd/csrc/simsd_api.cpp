@@ -39,10 +39,7 @@ extern "C" simsd_status simsd_verify_attention(
     a.num_ref = num_ref;
     a.out = out;
     a.lse = lse;
-    a.tickets = p.workspace ? static_cast<int32_t*>(workspace) : nullptr;
-    a.part = p.workspace
-                 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + p.ticket_bytes)
-                 : nullptr;
+    a.part = p.workspace ? static_cast<float*>(workspace) : nullptr;
     a.cs_seq = desc->cache_stride_seq;
     a.cs_tok = desc->cache_stride_token;
     a.cs_head = desc->cache_stride_head;
@@ -92,8 +89,7 @@ extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const
     a.confidence = confidence;
     a.draft_prob = draft_prob;
     a.accept_len = accept_len;
-    a.tickets = static_cast<int32_t*>(workspace);
-    a.part = reinterpret_cast<AcceptPartial*>(static_cast<char*>(workspace) + p.ticket_bytes);
+    a.part = static_cast<AcceptPartial*>(workspace);
     a.nvec = p.nvec;
     a.chunk_vecs = p.chunk_vecs;
     a.B = desc->block_size;

@@ -9,29 +9,33 @@
 //
 // Work decomposition: one work-group per (prefix chunk, KV head x row block,
 // sequence).  The G query heads of a KV head and all B+L new slots are packed
-// into the M rows of one row block (GQA packing), so each K/V byte of the
-// prefix is read from HBM once per KV head.  Chunks of one (sequence, KV head,
-// row block) write unnormalised partial outputs plus their running max and
-// sum; the last chunk to finish (counted with a per-pair ticket) merges them.
+// into the rows of one row block (GQA packing), so each K/V byte of the prefix
+// is read from HBM once per KV head.  When a sequence's prefix spans several
+// chunks, each chunk writes an unnormalised partial output with its running
+// max and sum, and a second kernel merges them; there is no device-wide fence
+// or counter in the streaming kernel.
 //
-// bf16 path: K and V tiles of 64 keys are staged through LDS.  Scores are
-// computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16, so lane l
-// owns query row l % 32 of its wave's 32-row block: the softmax state of a row
-// never leaves its two lanes (l, l ^ 32).  The PV product is likewise
-// transposed, O^T = V^T P^T, with P taken straight from the score registers as
-// the B operand; V is transposed on the fly (8 key rows x DPL dims per lane,
-// byte-permuted in registers).  Row maxima are kept in log2 units and only
-// rescaled when they grow by more than 2^8 (the exponentials stay <= 256).
+// bf16 path: K and V tiles of 64 keys are loaded into registers one tile ahead
+// (two ahead for 8-wave groups) and written to a double-buffered LDS ring with
+// 288-byte rows (no bank conflicts for the reads below).  Scores are computed
+// transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16, so lane l owns query
+// row l % 32 of its wave's 32-row block and a row's softmax state stays in two
+// lanes (l, l ^ 32).  O^T = V^T P^T takes P straight from the score registers
+// as the B operand; the V^T operand comes from LDS transpose reads
+// (ds_read_b64_tr_b16), so no register shuffles are needed.  Row maxima are
+// kept in log2 units and rescaled only when they grow by more than 2^8.
 #include "simsd_kernels.h"
 
 namespace simsd {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+#define SIMSD_LDS __attribute__((address_space(3)))
 
 constexpr float kLn2 = 0.69314718055994531f;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -87,7 +91,7 @@ __device__ inline uint32_t pack_bf16x2(float lo, float hi) {
   return bf16_bits(lo) | (bf16_bits(hi) << 16);
 }
 
-// Common prologue: which prefix keys this work-group owns.
+// Which prefix keys a work-group owns.
 struct Work {
   int split, kvh, rb, b, plen, nsplit, kbeg, kend, gamma;
 };
@@ -119,156 +123,78 @@ __device__ inline int64_t cache_offset(const AttnArgs& a, int b, int kvh, int ke
   return off + static_cast<int64_t>(kvh) * a.cs_head + e;
 }
 
-// Merge of the split partials of one (sequence, KV head, row block), run by
-// the last work-group to finish.  Partial layout per split: O[rows_pb][D]
-// (unnormalised), then m[rows_pb] (log2 units), then l[rows_pb].
-template <int D, int NT, typename OutT>
-__device__ void merge_splits(const AttnArgs& a, int64_t pair, const Work& w, const uint64_t* vis,
-                             int tid) {
-  constexpr int D4 = D / 4;
-  const int64_t pstride = static_cast<int64_t>(a.rows_pb) * (D + 2);
-  const float* base = a.part + pair * a.splits * pstride;
-  const int mo = a.rows_pb * D;
-  for (int idx = tid; idx < a.rows_pb * D4; idx += NT) {
-    const int rowl = idx / D4, d0 = (idx % D4) * 4;
-    const int m = w.rb * a.rows_pb + rowl;
-    if (m >= a.rows) continue;
-    const int t = m / a.group, hq = w.kvh * a.group + m % a.group;
-    const bool valid = vis[t] != 0ull;
-    float mt = kNegInf;
-    for (int s = 0; s < w.nsplit; ++s) mt = fmaxf(mt, base[s * pstride + mo + rowl]);
-    float lsum = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (valid && mt != kNegInf) {
-      for (int s = 0; s < w.nsplit; ++s) {
-        const float* ps = base + s * pstride;
-        const float wt = __builtin_amdgcn_exp2f(ps[mo + rowl] - mt);
-        lsum += wt * ps[mo + a.rows_pb + rowl];
-        acc += wt * *reinterpret_cast<const f32x4*>(ps + rowl * D + d0);
-      }
-    }
-    const bool ok = valid && lsum > 0.f;
-    const float inv = ok ? 1.f / lsum : 0.f;
-    const int64_t orow = ((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D + d0;
-    if constexpr (sizeof(OutT) == 2) {
-      u32x2 pk = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
-      *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.out) + orow) = pk;
-    } else {
-      *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = acc * inv;
-    }
-    if (d0 == 0 && a.lse)
-      a.lse[(static_cast<int64_t>(w.b) * a.hq + hq) * a.n_new + t] =
-          ok ? (mt + __log2f(lsum)) * kLn2 : kNegInf;
-  }
-}
-
-// Ticket protocol after a partial has been written.  Returns true in the one
-// work-group that must merge.  Release fence before the ticket, acquire after.
-__device__ inline bool arrive_last(const AttnArgs& a, int64_t pair, int nsplit, int* s_last) {
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) *s_last = (atomicAdd(a.tickets + pair, 1) == nsplit - 1);
-  __syncthreads();
-  if (!*s_last) return false;
-  __threadfence();
-  return true;
+// Partial layout per (pair, split): O[rows_pb][D] (unnormalised, fp32), then
+// m[rows_pb] (log2 units), then l[rows_pb].
+__device__ inline float* partial_base(const AttnArgs& a, const Work& w, int D) {
+  const int64_t pair = (static_cast<int64_t>(w.b) * a.hkv + w.kvh) * a.row_blocks + w.rb;
+  return a.part + (pair * a.splits + w.split) * static_cast<int64_t>(a.rows_pb) * (D + 2);
 }
 
 // ----------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ----------------------------------------------------------------------------
-template <int D, int NT, bool PAGED>
-__device__ inline void load_kv_tile(uint8_t* sk, uint8_t* sv, const AttnArgs& a, const Work& w,
-                                    int k0, bool is_new, int tid) {
-  constexpr int CH = D / 8;                  // 16-byte chunks per key row
-  constexpr int PER = kTile * CH / NT;       // chunks per thread
-  constexpr int ROWB = 2 * D + 16;           // padded LDS row (bytes)
-  static_assert(PER >= 1, "tile too small for the work-group");
-  u32x4 kr[PER], vr[PER];
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = tid + i * NT;
-    const int row = c / CH, e = (c % CH) * 8;
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    kr[i] = zero;
-    vr[i] = zero;
-    if (is_new) {
-      if (row < a.n_new) {
-        const int64_t off = ((static_cast<int64_t>(w.b) * a.n_new + row) * a.hkv + w.kvh) * D + e;
-        kr[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_new) + off);
-        vr[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_new) + off);
-      }
-    } else {
-      const int key = k0 + row;
-      if (key < w.kend) {
-        const int64_t off = cache_offset<PAGED>(a, w.b, w.kvh, key, e);
-        kr[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_cache) + off);
-        vr[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_cache) + off);
-      }
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = tid + i * NT;
-    const int row = c / CH, ch = c % CH;
-    *reinterpret_cast<u32x4*>(sk + row * ROWB + ch * 16) = kr[i];
-    *reinterpret_cast<u32x4*>(sv + row * ROWB + ch * 16) = vr[i];
-  }
-}
-
-// V^T operands for one 16-key chunk: lane (n, h) supplies keys
-// kappa(i) = kbase + 8*(i/4) + 4*h + i%4 (i < 8) at dims DPL*n + c, c < DPL.
 template <int D>
-__device__ inline void v_operands(const uint8_t* sv, int kbase, int n, int h,
-                                  bf16x8 (&va)[D / 32]) {
-  constexpr int DPL = D / 32;
-  constexpr int ROWB = 2 * D + 16;
-  if constexpr (DPL == 4) {
-    u32x2 r[8];
+struct TileGeom {
+  static constexpr int CH = D / 8;             // 16-byte chunks per key row
+  static constexpr int ROWB = 2 * D + 32;      // LDS bytes per key row (padded)
+  static constexpr int TILEB = kTile * ROWB;   // one tensor (K or V) of one tile
+};
+
+// Global -> registers for one 64-key tile: PER chunks of K and of V per thread.
+template <int D, int NT, bool PAGED>
+struct TileRegs {
+  static constexpr int PER = kTile * TileGeom<D>::CH / NT;
+  static_assert(PER >= 1, "tile too small for the work-group");
+  u32x4 k[PER], v[PER];
+
+  __device__ inline void load(const AttnArgs& a, const Work& w, int k0, bool is_new, int tid) {
+    constexpr int CH = TileGeom<D>::CH;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int key = kbase + 8 * (i >> 2) + 4 * h + (i & 3);
-      r[i] = *reinterpret_cast<const u32x2*>(sv + key * ROWB + n * 8);
-    }
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      u32x4 t;
-#pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const uint32_t lo = (c < 2) ? r[2 * p][0] : r[2 * p][1];
-        const uint32_t hi = (c < 2) ? r[2 * p + 1][0] : r[2 * p + 1][1];
-        t[p] = __builtin_amdgcn_perm(hi, lo, (c & 1) ? 0x07060302u : 0x05040100u);
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      const int row = c / CH, e = (c % CH) * 8;
+      const u32x4 zero = {0u, 0u, 0u, 0u};
+      k[i] = zero;
+      v[i] = zero;
+      if (is_new) {
+        if (row < a.n_new) {
+          const int64_t off = ((static_cast<int64_t>(w.b) * a.n_new + row) * a.hkv + w.kvh) * D + e;
+          k[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_new) + off);
+          v[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_new) + off);
+        }
+      } else {
+        const int key = k0 + row;
+        if (key < w.kend) {
+          const int64_t off = cache_offset<PAGED>(a, w.b, w.kvh, key, e);
+          k[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_cache) + off);
+          v[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_cache) + off);
+        }
       }
-      va[c] = __builtin_bit_cast(bf16x8, t);
-    }
-  } else {
-    uint32_t r[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int key = kbase + 8 * (i >> 2) + 4 * h + (i & 3);
-      r[i] = *reinterpret_cast<const uint32_t*>(sv + key * ROWB + n * 4);
-    }
-#pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      u32x4 t;
-#pragma unroll
-      for (int p = 0; p < 4; ++p)
-        t[p] = __builtin_amdgcn_perm(r[2 * p + 1], r[2 * p], c ? 0x07060302u : 0x05040100u);
-      va[c] = __builtin_bit_cast(bf16x8, t);
     }
   }
-}
+
+  __device__ inline void store(uint8_t* sk, uint8_t* sv, int tid) const {
+    constexpr int CH = TileGeom<D>::CH, ROWB = TileGeom<D>::ROWB;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * NT;
+      const int row = c / CH, ch = c % CH;
+      *reinterpret_cast<u32x4*>(sk + row * ROWB + ch * 16) = k[i];
+      *reinterpret_cast<u32x4*>(sv + row * ROWB + ch * 16) = v[i];
+    }
+  }
+};
 
 template <int D, int NW, bool PAGED>
-__global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
+__global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   constexpr int NT = NW * 64;
-  constexpr int DPL = D / 32;
-  constexpr int KS = D / 16;
-  constexpr int ROWB = 2 * D + 16;
-  __shared__ __attribute__((aligned(16))) uint8_t sk[kTile * ROWB];
-  __shared__ __attribute__((aligned(16))) uint8_t sv[kTile * ROWB];
+  constexpr int NB = D / 32;                   // 32-dim output blocks
+  constexpr int KS = D / 16;                   // k-steps of QK^T
+  constexpr int ROWB = TileGeom<D>::ROWB;
+  constexpr int TILEB = TileGeom<D>::TILEB;
+  constexpr int PF = NW >= 8 ? 2 : 1;          // tiles prefetched into registers
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2][2][TILEB];   // [buffer][K, V]
   __shared__ uint64_t vis[kMaxNew];
-  __shared__ int s_last;
 
   Work w;
   if (!setup_work(a, w)) return;
@@ -277,6 +203,18 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
   const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
   if (tid < kMaxNew)
     vis[tid] = tid < a.n_new ? visibility_word(tid, step_row, w.gamma, a.B, a.n_new) : 0ull;
+
+  const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
+  const int nt = ntp + (w.split == 0 ? 1 : 0);
+  auto tile_k0 = [&](int it) { return w.kbeg + it * kTile; };
+
+  // Start streaming before anything else.
+  TileRegs<D, NT, PAGED> regs[PF];
+  regs[0].load(a, w, tile_k0(0), 0 == ntp, tid);
+  regs[0].store(smem[0][0], smem[0][1], tid);
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (1 + p < nt) regs[(1 + p) % PF].load(a, w, tile_k0(1 + p), 1 + p == ntp, tid);
 
   const int rowl = wave * 32 + n;
   const int m = w.rb * a.rows_pb + rowl;
@@ -302,22 +240,30 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
   __syncthreads();
   const uint64_t myvis = row_in ? vis[t] : 0ull;
 
-  f32x16 o[DPL];
+  f32x16 o[NB];
 #pragma unroll
-  for (int c = 0; c < DPL; ++c)
+  for (int c = 0; c < NB; ++c)
 #pragma unroll
     for (int j = 0; j < 16; ++j) o[c][j] = 0.f;
   float m_run = kNegInf, l_run = 0.f;
   const float sl2 = a.scale_log2;
 
-  const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
-  const int nt = ntp + (w.split == 0 ? 1 : 0);
-  for (int it = 0; it < nt; ++it) {
+  // Transpose-read addressing: lane (g = lane/16, k = (lane%16)/4, q = lane%4)
+  // reads 4 dims at column 16*(g%2) + 4*q of key row 4*h + k.
+  const int tr_row = 4 * h + ((lane & 15) >> 2);
+  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+
+  // The loop is unrolled by PF so that every register-set index is a
+  // compile-time constant (a runtime index would put the sets in scratch).
+  for (int it0 = 0; it0 < nt; it0 += PF) {
+#pragma unroll
+  for (int u = 0; u < PF; ++u) {
+    const int it = it0 + u;
+    if (it >= nt) break;
     const bool is_new = it == ntp;
-    const int k0 = w.kbeg + it * kTile;
-    if (it > 0) __syncthreads();
-    load_kv_tile<D, NT, PAGED>(sk, sv, a, w, k0, is_new, tid);
-    __syncthreads();
+    const int k0 = tile_k0(it);
+    const uint8_t* sk = smem[it & 1][0];
+    const uint8_t* sv = smem[it & 1][1];
 
     // S^T = K Q^T: two 32-key blocks.  Register j of block kb holds key
     // 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
@@ -362,7 +308,7 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
-      for (int c = 0; c < DPL; ++c) o[c] *= alpha;
+      for (int c = 0; c < NB; ++c) o[c] *= alpha;
       m_run = m_new;
     }
     const float moff = m_run == kNegInf ? 0.f : m_run;
@@ -375,7 +321,8 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
         l_run += p;
       }
 
-    // O^T += V^T P^T, one 16-key chunk at a time.
+    // O^T += V^T P^T, one 16-key chunk at a time.  Chunk (kb, hf) covers keys
+    // 32*kb + 16*hf + kappa(h, i), kappa(h, i) = 8*(i/4) + 4*h + i%4.
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -384,73 +331,63 @@ __global__ void __launch_bounds__(NW * 64) attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int p = 0; p < 4; ++p) pw[p] = pack_bf16x2(s[kb][8 * hf + 2 * p], s[kb][8 * hf + 2 * p + 1]);
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-        bf16x8 va[DPL];
-        v_operands<D>(sv, 32 * kb + 16 * hf, n, h, va);
+        const uint8_t* vrow = sv + (32 * kb + 16 * hf + tr_row) * ROWB + tr_col * 2;
 #pragma unroll
-        for (int c = 0; c < DPL; ++c)
-          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[c], pb, o[c], 0, 0, 0);
+        for (int c = 0; c < NB; ++c) {
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (SIMSD_LDS s16x4*)(vrow + 64 * c));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (SIMSD_LDS s16x4*)(vrow + 8 * ROWB + 64 * c));
+          const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
+          const u32x4 vw = {l2[0], l2[1], h2[0], h2[1]};
+          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb, o[c], 0, 0, 0);
+        }
       }
+
+    // Next tile: registers -> the other LDS buffer, then refill the registers.
+    if (it + 1 < nt) {
+      regs[(u + 1) % PF].store(smem[(it + 1) & 1][0], smem[(it + 1) & 1][1], tid);
+      if (it + 1 + PF < nt)
+        regs[(u + 1) % PF].load(a, w, tile_k0(it + 1 + PF), it + 1 + PF == ntp, tid);
+    }
+    __syncthreads();
+  }
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (!row_in) return;
 
-  // Register j of o[c] holds dim DPL*(8*(j/4) + 4*h + j%4) + c of this row.
+  // Register j of o[c] holds dim 32*c + 8*(j/4) + 4*h + j%4 of this row.
   if (w.nsplit == 1) {
-    if (!row_in) return;
     const bool valid = myvis != 0ull;
     const float inv = valid ? 1.f / l_tot : 0.f;
     uint16_t* orow = static_cast<uint16_t*>(a.out) +
                      ((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      if constexpr (DPL == 4) {
-        u32x4 lo, hi;
+    for (int c = 0; c < NB; ++c)
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-          lo[2 * jj] = pack_bf16x2(o[0][4 * q + jj] * inv, o[1][4 * q + jj] * inv);
-          lo[2 * jj + 1] = pack_bf16x2(o[2][4 * q + jj] * inv, o[3][4 * q + jj] * inv);
-          hi[2 * jj] = pack_bf16x2(o[0][4 * q + 2 + jj] * inv, o[1][4 * q + 2 + jj] * inv);
-          hi[2 * jj + 1] = pack_bf16x2(o[2][4 * q + 2 + jj] * inv, o[3][4 * q + 2 + jj] * inv);
-        }
-        *reinterpret_cast<u32x4*>(orow + 32 * q + 16 * h) = lo;
-        *reinterpret_cast<u32x4*>(orow + 32 * q + 16 * h + 8) = hi;
-      } else {
-        u32x4 v;
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) v[jj] = pack_bf16x2(o[0][4 * q + jj] * inv, o[1][4 * q + jj] * inv);
-        *reinterpret_cast<u32x4*>(orow + 16 * q + 8 * h) = v;
+      for (int q = 0; q < 4; ++q) {
+        const u32x2 v = {pack_bf16x2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
+                         pack_bf16x2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
+        *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * q + 4 * h) = v;
       }
-    }
     if (a.lse && h == 0)
       a.lse[(static_cast<int64_t>(w.b) * a.hq + hq) * a.n_new + t] =
           valid ? (m_run + __log2f(l_tot)) * kLn2 : kNegInf;
     return;
   }
-
-  const int64_t pair = (static_cast<int64_t>(w.b) * a.hkv + w.kvh) * a.row_blocks + w.rb;
-  float* part = a.part + (pair * a.splits + w.split) * static_cast<int64_t>(a.rows_pb) * (D + 2);
-  if (row_in) {
-    float* prow = part + rowl * D;
+  float* part = partial_base(a, w, D);
+  float* prow = part + rowl * D;
+#pragma unroll
+  for (int c = 0; c < NB; ++c)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        if constexpr (DPL == 4) {
-          const f32x4 v = {o[0][4 * q + jj], o[1][4 * q + jj], o[2][4 * q + jj], o[3][4 * q + jj]};
-          *reinterpret_cast<f32x4*>(prow + 32 * q + 16 * h + 4 * jj) = v;
-        } else if (jj % 2 == 0) {
-          const f32x4 v = {o[0][4 * q + jj], o[1][4 * q + jj], o[0][4 * q + jj + 1], o[1][4 * q + jj + 1]};
-          *reinterpret_cast<f32x4*>(prow + 16 * q + 8 * h + 2 * jj) = v;
-        }
-      }
+      const f32x4 v = {o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
+      *reinterpret_cast<f32x4*>(prow + 32 * c + 8 * q + 4 * h) = v;
     }
-    if (h == 0) {
-      part[a.rows_pb * D + rowl] = m_run;
-      part[a.rows_pb * D + a.rows_pb + rowl] = l_tot;
-    }
+  if (h == 0) {
+    part[a.rows_pb * D + rowl] = m_run;
+    part[a.rows_pb * D + a.rows_pb + rowl] = l_tot;
   }
-  if (!arrive_last(a, pair, w.nsplit, &s_last)) return;
-  merge_splits<D, NT, uint16_t>(a, pair, w, vis, tid);
-  if (tid == 0) atomicExch(a.tickets + pair, 0);
 }
 
 // ----------------------------------------------------------------------------
@@ -468,7 +405,6 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
   __shared__ float so[32 * D];
   __shared__ float sm[32], sl[32];
   __shared__ uint64_t vis[kMaxNew];
-  __shared__ int s_last;
 
   Work w;
   if (!setup_work(a, w)) return;
@@ -575,28 +511,84 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
     }
     return;
   }
-  const int64_t pair = (static_cast<int64_t>(w.b) * a.hkv + w.kvh) * a.row_blocks + w.rb;
-  float* part = a.part + (pair * a.splits + w.split) * static_cast<int64_t>(a.rows_pb) * (D + 2);
+  float* part = partial_base(a, w, D);
   for (int idx = tid; idx < 32 * D; idx += NT) part[idx] = so[idx];
   if (tid < 32) {
     part[a.rows_pb * D + tid] = sm[tid];
     part[a.rows_pb * D + a.rows_pb + tid] = sl[tid];
   }
-  if (!arrive_last(a, pair, w.nsplit, &s_last)) return;
-  merge_splits<D, NT, float>(a, pair, w, vis, tid);
-  if (tid == 0) atomicExch(a.tickets + pair, 0);
+}
+
+// ----------------------------------------------------------------------------
+// Merge of split partials.  Grid: (32-row groups of a row block, KV head x row
+// block, sequence); one thread per (row, 4 dims).  Sequences whose prefix fits
+// one chunk were finished by the attention kernel and are skipped.
+// ----------------------------------------------------------------------------
+template <int D, typename OutT>
+__global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
+  constexpr int D4 = D / 4;
+  const int b = blockIdx.z;
+  const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
+  const int plen = min(max(a.prefix_lens[b], 0), a.max_prefix);
+  const int nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
+  if (nsplit <= 1) return;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  const int rowl = idx / D4, d0 = (idx % D4) * 4;
+  if (rowl >= a.rows_pb) return;
+  const int m = rb * a.rows_pb + rowl;
+  if (m >= a.rows) return;
+  const int t = m / a.group, hq = kvh * a.group + m % a.group;
+  const int gamma = min(max(a.num_ref[b], 0), a.L);
+  // A row is padding iff it sees no new slot (a non-padded row always sees itself).
+  bool valid;
+  if (t < a.B) valid = a.step_map[static_cast<int64_t>(b) * a.B + t] >= 0;
+  else valid = (t - a.B) < gamma;
+
+  const int64_t pair = (static_cast<int64_t>(b) * a.hkv + kvh) * a.row_blocks + rb;
+  const int64_t pstride = static_cast<int64_t>(a.rows_pb) * (D + 2);
+  const float* base = a.part + pair * a.splits * pstride;
+  const int mo = a.rows_pb * D;
+  float mt = kNegInf;
+  for (int s = 0; s < nsplit; ++s) mt = fmaxf(mt, base[s * pstride + mo + rowl]);
+  float lsum = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  if (valid && mt != kNegInf) {
+#pragma unroll 4
+    for (int s = 0; s < nsplit; ++s) {
+      const float* ps = base + s * pstride;
+      const float wt = __builtin_amdgcn_exp2f(ps[mo + rowl] - mt);
+      lsum += wt * ps[mo + a.rows_pb + rowl];
+      acc += wt * *reinterpret_cast<const f32x4*>(ps + rowl * D + d0);
+    }
+  }
+  const bool ok = valid && lsum > 0.f;
+  const float inv = ok ? 1.f / lsum : 0.f;
+  const int64_t orow = ((static_cast<int64_t>(b) * a.n_new + t) * a.hq + hq) * D + d0;
+  if constexpr (sizeof(OutT) == 2) {
+    const u32x2 pk = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
+    *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.out) + orow) = pk;
+  } else {
+    *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = acc * inv;
+  }
+  if (d0 == 0 && a.lse)
+    a.lse[(static_cast<int64_t>(b) * a.hq + hq) * a.n_new + t] =
+        ok ? (mt + __log2f(lsum)) * kLn2 : kNegInf;
 }
 
 template <int D, bool PAGED>
-hipError_t launch_bf16(int waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
+void launch_bf16(int waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
   switch (waves) {
     case 1: hipLaunchKernelGGL((attn_bf16_kernel<D, 1, PAGED>), grid, dim3(64), 0, st, a); break;
     case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, PAGED>), grid, dim3(128), 0, st, a); break;
     case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, PAGED>), grid, dim3(256), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, PAGED>), grid, dim3(512), 0, st, a); break;
-    default: return hipErrorInvalidValue;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, PAGED>), grid, dim3(512), 0, st, a); break;
   }
-  return hipGetLastError();
+}
+
+template <int D>
+void launch_f32(bool paged, dim3 grid, const AttnArgs& a, hipStream_t st) {
+  if (paged) hipLaunchKernelGGL((attn_f32_kernel<D, true>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((attn_f32_kernel<D, false>), grid, dim3(256), 0, st, a);
 }
 
 }  // namespace
@@ -606,18 +598,28 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const dim3 grid(p.splits, d.num_kv_heads * p.row_blocks, d.batch);
   const bool paged = d.page_size > 0;
   if (d.dtype == SIMSD_BF16) {
-    if (d.head_dim == 128)
-      return paged ? launch_bf16<128, true>(p.waves, grid, a, st)
-                   : launch_bf16<128, false>(p.waves, grid, a, st);
-    return paged ? launch_bf16<64, true>(p.waves, grid, a, st)
-                 : launch_bf16<64, false>(p.waves, grid, a, st);
-  }
-  if (d.head_dim == 128) {
-    if (paged) hipLaunchKernelGGL((attn_f32_kernel<128, true>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((attn_f32_kernel<128, false>), grid, dim3(256), 0, st, a);
+    if (d.head_dim == 128) {
+      if (paged) launch_bf16<128, true>(p.waves, grid, a, st);
+      else launch_bf16<128, false>(p.waves, grid, a, st);
+    } else {
+      if (paged) launch_bf16<64, true>(p.waves, grid, a, st);
+      else launch_bf16<64, false>(p.waves, grid, a, st);
+    }
   } else {
-    if (paged) hipLaunchKernelGGL((attn_f32_kernel<64, true>), grid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((attn_f32_kernel<64, false>), grid, dim3(256), 0, st, a);
+    if (d.head_dim == 128) launch_f32<128>(paged, grid, a, st);
+    else launch_f32<64>(paged, grid, a, st);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || p.splits <= 1) return e;
+  const int per_block = (p.rows_pb * d.head_dim / 4 + 255) / 256;
+  const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
+  const bool bf16 = d.dtype == SIMSD_BF16;
+  if (d.head_dim == 128) {
+    if (bf16) hipLaunchKernelGGL((merge_kernel<128, uint16_t>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<128, float>), mgrid, dim3(256), 0, st, a);
+  } else {
+    if (bf16) hipLaunchKernelGGL((merge_kernel<64, uint16_t>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, float>), mgrid, dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }

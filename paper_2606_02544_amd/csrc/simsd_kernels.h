@@ -22,7 +22,6 @@ struct AttnArgs {
   void* out;
   float* lse;
   float* part;        // split partials (workspace), or null when splits == 1
-  int32_t* tickets;   // one completion counter per (sequence, KV head, row block)
   int64_t cs_seq, cs_tok, cs_head;
   int hq, hkv, group, B, L, n_new, rows, rows_pb, row_blocks;
   int page_size, max_pages, chunk, splits, max_prefix;
@@ -39,7 +38,6 @@ struct AcceptArgs {
   float* draft_prob;
   int32_t* accept_len;
   AcceptPartial* part;
-  int32_t* tickets;
   int64_t nvec, chunk_vecs;
   int B, L, V, cpr;
 };

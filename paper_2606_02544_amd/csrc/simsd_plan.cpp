@@ -81,23 +81,19 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   if (d->kv_chunk > 0) {
     r.chunk = d->kv_chunk;
   } else {
-    // Split the longest prefix so that about kTargetUnits work-groups exist.
-    int64_t c = ceil_div(static_cast<int64_t>(d->max_prefix_len) * r.pairs, kTargetUnits);
+    // Split the longest prefix so that about as many work-groups exist as the
+    // chip holds at once: one 8-wave group or two smaller groups per CU.
+    const int64_t target = r.waves >= 8 ? kCUs : 2 * kCUs;
+    int64_t c = ceil_div(static_cast<int64_t>(d->max_prefix_len) * r.pairs, target);
     c = ceil_div(c, kTile) * kTile;
-    if (c < kTile) c = kTile;
+    if (c < kMinAutoChunk) c = kMinAutoChunk;
     if (c > kMaxAutoChunk) c = kMaxAutoChunk;
     r.chunk = static_cast<int>(c);
   }
   r.splits = d->max_prefix_len > 0 ? static_cast<int>(ceil_div(d->max_prefix_len, r.chunk)) : 1;
   if (r.splits > 65535 * 1024) return fail(SIMSD_ERR_BAD_SHAPE, "attention: too many splits");
   r.part_floats = static_cast<size_t>(r.rows_pb) * (d->head_dim + 2);
-  if (r.splits > 1) {
-    r.ticket_bytes = static_cast<size_t>(ceil_div(r.pairs * 4, 256) * 256);
-    r.workspace = r.ticket_bytes + static_cast<size_t>(r.pairs) * r.splits * r.part_floats * 4;
-  } else {
-    r.ticket_bytes = 0;
-    r.workspace = 0;
-  }
+  r.workspace = r.splits > 1 ? static_cast<size_t>(r.pairs) * r.splits * r.part_floats * 4 : 0;
   const float scale = d->scale > 0.f ? d->scale : 1.0f / std::sqrt(static_cast<float>(d->head_dim));
   r.scale_log2 = scale * 1.4426950408889634f;
   *p = r;
@@ -161,8 +157,7 @@ simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p) {
   if (cpr > 65535 * 1024) return fail(SIMSD_ERR_BAD_SHAPE, "accept: chunks_per_row too large");
   r.cpr = static_cast<int>(cpr);
   r.chunk_vecs = ceil_div(r.nvec, r.cpr);
-  r.ticket_bytes = static_cast<size_t>(ceil_div(static_cast<int64_t>(d->batch) * 4, 256) * 256);
-  r.workspace = r.ticket_bytes + static_cast<size_t>(rows) * r.cpr * sizeof(AcceptPartial);
+  r.workspace = static_cast<size_t>(rows) * r.cpr * sizeof(AcceptPartial);
   *p = r;
   return SIMSD_OK;
 }

@@ -13,8 +13,9 @@ namespace simsd {
 constexpr int kTile = 64;            // keys per attention tile
 constexpr int kMaxNew = 64;          // B + L limit (one 64-bit visibility word per row)
 constexpr int kMaxGroup = 16;        // Hq / Hkv limit
-constexpr int kTargetUnits = 512;    // work-groups the split heuristic aims for (2 per CU)
-constexpr int kMaxAutoChunk = 4096;  // longest automatic prefix chunk (keys)
+constexpr int kCUs = 256;            // compute units of an MI355X
+constexpr int kMinAutoChunk = 128;   // shortest automatic prefix chunk (keys)
+constexpr int kMaxAutoChunk = 8192;  // longest automatic prefix chunk (keys)
 constexpr int kAcceptThreads = 256;  // threads of the vocabulary-scan work-group
 constexpr int kAcceptTarget = 2048;  // scan work-groups the chunk heuristic aims for
 
@@ -27,9 +28,8 @@ struct AttnPlan {
   int row_blocks = 0;   // ceil(rows / rows_pb)
   int chunk = 0;        // prefix keys per split
   int splits = 0;       // grid.x: ceil(max_prefix_len / chunk), >= 1
-  int64_t pairs = 0;    // batch * Hkv * row_blocks (one ticket each)
+  int64_t pairs = 0;    // batch * Hkv * row_blocks
   size_t part_floats = 0;   // floats per split partial: rows_pb * (head_dim + 2)
-  size_t ticket_bytes = 0;  // bytes reserved for tickets at the start of the workspace
   size_t workspace = 0;     // total bytes
   float scale_log2 = 0.f;   // softmax scale * log2(e)
 };
@@ -39,7 +39,6 @@ struct AcceptPlan {
   int64_t nvec = 0;       // vectors per row
   int cpr = 0;            // chunks (work-groups) per row
   int64_t chunk_vecs = 0; // vectors per chunk
-  size_t ticket_bytes = 0;
   size_t workspace = 0;
 };
 

@@ -63,17 +63,18 @@ def cfg_desc(cid, **kw):
 
 
 def test_workspace_sizes_follow_the_plan():
-    # config 4: 16 x 8 pairs, 256 packed rows, chunk 4096 -> 4 splits;
-    # 256-byte ticket block + 128 * 4 partials of 256 rows x (128 + 2) floats.
-    assert binding.attention_workspace_size(cfg_desc(4)) == 512 + 128 * 4 * 256 * 130 * 4
+    # config 4: 16 x 8 pairs, 256 packed rows in 8 waves -> chunk 8192 -> 2 splits;
+    # 128 * 2 partials of 256 rows x (128 + 2) floats.
+    assert binding.attention_workspace_size(cfg_desc(4)) == 128 * 2 * 256 * 130 * 4
+    assert binding.attention_workspace_size(cfg_desc(4, kv_chunk=4096)) == 128 * 4 * 256 * 130 * 4
     # a single split needs no workspace
     assert binding.attention_workspace_size(cfg_desc(1, kv_chunk=64)) == 0
     assert binding.attention_workspace_size(cfg_desc(2)) > 0
     assert binding.attention_workspace_size(cfg_desc(1, head_dim=96)) == 0   # invalid -> 0
     acc = AcceptDesc(batch=16, block_size=32, max_ref=32, vocab=151936, chunks_per_row=0,
                      logits_dtype=binding.SIMSD_BF16)
-    # 512 rows -> 4 chunks per row; 256-byte tickets + 16-byte partials
-    assert binding.accept_workspace_size(acc) == 256 + 512 * 4 * 16
+    # 512 rows -> 4 chunks per row; 16-byte partials
+    assert binding.accept_workspace_size(acc) == 512 * 4 * 16
 
 
 def call_attention(desc, **over):
