@@ -140,6 +140,10 @@ def main():
     ap.add_argument("--rotate-mb", type=float, default=640.0,
                     help="cycle input copies until this many MB are touched per cycle")
     ap.add_argument("--kv-chunk", type=int, default=0)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch every kernel from Python instead of replaying HIP graphs")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
+                    help="only copy MB megabytes a few times (counter calibration) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -149,6 +153,15 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        n = args.copy_probe * 1000 * 1000
+        x = torch.ones(n, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        for _ in range(5):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "launches": 5}))
+        return
     from paper_2606_02544_amd import binding
     from synth import CONFIGS, generate
 
@@ -199,55 +212,100 @@ def main():
 
     lib = binding.lib()
     P = ctypes.c_void_p
-    stream = torch.cuda.current_stream()
-    sp = P(stream.cuda_stream)
     ptr = lambda t: None if t is None else P(t.data_ptr())
-    calls = []
-    for s in sets:
-        a_args = (ctypes.byref(adesc), ptr(s["q"]), ptr(s["k_new"]), ptr(s["v_new"]),
-                  ptr(s["k_cache"]), ptr(s["v_cache"]), ptr(s["block_table"]),
-                  ptr(s["prefix_lens"]), ptr(s["step_map"]), ptr(s["num_ref"]), ptr(out),
-                  ptr(lse), ptr(aws), aws_n, sp)
-        c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]), ptr(s["step_map"]),
-                  ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob), ptr(alen), ptr(cws),
-                  cws_n, sp)
-        calls.append((a_args, c_args))
+
+    def build_calls(stream):
+        """ctypes argument tuples of both entry points for every input copy."""
+        sp = P(stream.cuda_stream)
+        out_calls = []
+        for s in sets:
+            a_args = (ctypes.byref(adesc), ptr(s["q"]), ptr(s["k_new"]), ptr(s["v_new"]),
+                      ptr(s["k_cache"]), ptr(s["v_cache"]), ptr(s["block_table"]),
+                      ptr(s["prefix_lens"]), ptr(s["step_map"]), ptr(s["num_ref"]), ptr(out),
+                      ptr(lse), ptr(aws), aws_n, sp)
+            c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]),
+                      ptr(s["step_map"]), ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob),
+                      ptr(alen), ptr(cws), cws_n, sp)
+            out_calls.append((a_args, c_args))
+        return out_calls
+
+    calls = build_calls(torch.cuda.current_stream())
     f_attn, f_acc = lib.simsd_verify_attention, lib.simsd_verify_accept
 
-    def step(i):
+    def launch_step(i, what=("attn", "acc")):
         a_args, c_args = calls[i % len(calls)]
-        st = f_attn(*a_args)
-        st |= f_acc(*c_args)
-        return st
-
-    print(f"[bench] {cfg.name}: {copies} input copies, {step_bytes / 1e6:.1f} MB per step; "
-          f"warmup {args.warmup}", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        if step(i):
+        st = 0
+        if "attn" in what:
+            st |= f_attn(*a_args)
+        if "acc" in what:
+            st |= f_acc(*c_args)
+        if st:
             raise RuntimeError(lib.simsd_last_error().decode())
-    torch.cuda.synchronize()
 
-    K = args.steps
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    K, W = args.steps, args.warmup
+    print(f"[bench] {cfg.name}: {copies} input copies, {step_bytes / 1e6:.1f} MB per step; "
+          f"warmup {W}, steps {K}, hip graph {not args.no_graph}", file=sys.stderr, flush=True)
+    graphs = {}
+    use_graph = not args.no_graph
+    if use_graph:
+        # One graph per sequence of launches: the K timed steps, the warmup, and
+        # attention-only / accept-only passes over every input copy for the
+        # per-kernel durations.  The library never allocates or synchronises,
+        # so its launches capture as they are.
+        cap = torch.cuda.Stream()
+        eager_calls = calls
+        calls = build_calls(cap)
+        with torch.cuda.stream(cap):
+            launch_step(0)
+            torch.cuda.synchronize()
+            for name, n, what in (("warm", W, ("attn", "acc")), ("steps", K, ("attn", "acc")),
+                                  ("attn", copies, ("attn",)), ("acc", copies, ("acc",))):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    for i in range(n):
+                        launch_step(i, what)
+                graphs[name] = g
+        torch.cuda.synchronize()
+        calls = eager_calls
+
+    def run(name, n, what=("attn", "acc")):
+        if use_graph:
+            graphs[name].replay()
+        else:
+            for i in range(n):
+                launch_step(i, what)
+
+    run("warm", W)
+    torch.cuda.synchronize()
     print(f"[bench] timing {K} steps", file=sys.stderr, flush=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(K):
-        e0, e1, e2 = ev[i]
-        a_args, c_args = calls[i % len(calls)]
-        e0.record(stream)
-        f_attn(*a_args)
-        e1.record(stream)
-        f_acc(*c_args)
-        e2.record(stream)
+    run("steps", K)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     elapsed = t1 - t0
-    attn_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    acc_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+
+    # Average duration of each entry point: HIP events on the launch stream
+    # around back-to-back launches over every input copy (cold inputs).
+    def per_launch_ms(name, what, reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        run(name, copies, what)
+        torch.cuda.synchronize()
+        e0.record(torch.cuda.current_stream())
+        for _ in range(reps):
+            run(name, copies, what)
+        e1.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * copies)
+
+    reps = max(1, math.ceil(50 / copies))
+    attn_ms = per_launch_ms("attn", ("attn",), reps)
+    acc_ms = per_launch_ms("acc", ("acc",), reps)
+    # leave the outputs of the last timed step in place for the parity check
+    run("steps", K)
+    torch.cuda.synchronize()
     print(f"[bench] done: {elapsed / K * 1e3:.4f} ms/step (attention {attn_ms * 1e3:.2f} us, "
-          f"accept {acc_ms * 1e3:.2f} us)", file=sys.stderr, flush=True)
+          f"accept {acc_ms * 1e3:.2f} us per launch)", file=sys.stderr, flush=True)
 
     parity = None
     if not args.no_check:
@@ -298,7 +356,7 @@ def main():
             "accept_gbs": wl["accept_bytes"] / (acc_ms * 1e-3) / 1e9,
             "attention_mfma_frac": wl["attn_flops"] / (attn_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
             "input_copies": copies,
-            "hip_graph": False,
+            "hip_graph": use_graph,
             "kv_chunk": args.kv_chunk,
         },
         "roofline": {

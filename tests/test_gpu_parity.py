@@ -117,8 +117,7 @@ def test_split_count_invariance_and_determinism():
 
 
 def test_workspace_reuse_many_launches():
-    """Completion tickets return to zero: repeated launches on one workspace
-    keep producing the same result."""
+    """Repeated launches sharing one workspace keep producing the same bits."""
     inp = generate(CONFIGS[2], seed=5)
     d = DeviceInputs(inp)
     first = run_attention(d, 64)
@@ -176,3 +175,48 @@ def test_accept_bench_shape_chunking():
     ref = oracle_accept(inp)
     for cpr in (1, 7, 64, 0):
         check_accept(run_accept(d, cpr), ref)
+
+
+def test_hip_graph_replays_match_eager():
+    """Both entry points captured in one HIP graph (the benchmark's timing
+    mode): every replay, with eager work and synchronisation in between,
+    reproduces the eager outputs bit for bit."""
+    from paper_2606_02544_amd import binding
+    inp = generate(CONFIGS[3].replace(batch=2, prefix=700), seed=3, poison=True)
+    d = DeviceInputs(inp)
+    cfg = inp.cfg
+    kw = dict(block_size=cfg.block_size, max_ref=cfg.max_ref, max_prefix_len=cfg.max_prefix,
+              kv_chunk=128)
+    args = (d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_table, d.prefix_lens,
+            d.step_map, d.num_ref)
+    eager_out, eager_lse = binding.verify_attention(*args, **kw)
+    eager_acc = binding.verify_accept(d.logits, d.draft_ids, d.step_map, d.num_ref)
+    torch.cuda.synchronize()
+    out = torch.zeros_like(eager_out)
+    lse = torch.zeros_like(eager_lse)
+    acc = [torch.zeros_like(t) for t in eager_acc]
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        binding.verify_attention(*args, out=out, lse=lse, stream=s, **kw)   # workspaces exist
+        binding.verify_accept(d.logits, d.draft_ids, d.step_map, d.num_ref, target_ids=acc[0],
+                              confidence=acc[1], draft_prob=acc[2], accept_len=acc[3], stream=s)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            binding.verify_attention(*args, out=out, lse=lse, stream=s, **kw)
+            binding.verify_accept(d.logits, d.draft_ids, d.step_map, d.num_ref,
+                                  target_ids=acc[0], confidence=acc[1], draft_prob=acc[2],
+                                  accept_len=acc[3], stream=s)
+    for rep in range(4):
+        out.zero_()
+        lse.zero_()
+        for t in acc:
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager_out) and torch.equal(lse, eager_lse), rep
+        for a, b in zip(acc, eager_acc):
+            assert torch.equal(a, b), rep
+        binding.verify_attention(*args, **kw)       # eager work between replays
+        torch.cuda.synchronize()
