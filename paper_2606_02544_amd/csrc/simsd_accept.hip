@@ -201,24 +201,24 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
       a.confidence[static_cast<int64_t>(b) * a.B + tid] = scanned ? 1.f / s_row[tid].sm : 0.f;
   }
   __syncthreads();
-  if (a.draft_prob && tid < a.L) {
+  // One lane per draft r: its verification row, match flag and probability.
+  // The accepted prefix ends at the first rejected draft (a wave ballot).
+  if (wave == 0) {
+    const int r = lane;
+    bool rejected = false;
     float p = 0.f;
-    const int kr = tid < gamma ? s_row_of_step[tid] : -1;
-    const int tok = tid < gamma ? a.draft_ids[static_cast<int64_t>(b) * a.L + tid] : -1;
-    if (kr >= 0 && tok >= 0 && tok < a.V) {
-      const float x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
-      p = __builtin_amdgcn_exp2f((x - s_row[kr].mx) * kLog2e) / s_row[kr].sm;
+    if (r < gamma) {
+      const int kr = s_row_of_step[r];
+      const int tok = a.draft_ids[static_cast<int64_t>(b) * a.L + r];
+      rejected = kr < 0 || s_row[kr].ix != tok;
+      if (kr >= 0 && tok >= 0 && tok < a.V) {
+        const float x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
+        p = __builtin_amdgcn_exp2f((x - s_row[kr].mx) * kLog2e) / s_row[kr].sm;
+      }
     }
-    a.draft_prob[static_cast<int64_t>(b) * a.L + tid] = p;
-  }
-  if (tid == 0) {
-    int acc = 0;
-    while (acc < gamma) {
-      const int kr = s_row_of_step[acc];
-      if (kr < 0 || s_row[kr].ix != a.draft_ids[static_cast<int64_t>(b) * a.L + acc]) break;
-      ++acc;
-    }
-    a.accept_len[b] = acc;
+    if (a.draft_prob && r < a.L) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = p;
+    const unsigned long long rej = __ballot(rejected);
+    if (lane == 0) a.accept_len[b] = rej ? __ffsll(static_cast<long long>(rej)) - 1 : gamma;
   }
 }
 

@@ -84,12 +84,6 @@ __device__ uint64_t visibility_word(int i, const int32_t* step_row, int gamma, i
   return w;
 }
 
-__device__ inline uint32_t bf16_bits(float x) {
-  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<__bf16>(x)));
-}
-__device__ inline uint32_t pack_bf16x2(float lo, float hi) {
-  return bf16_bits(lo) | (bf16_bits(hi) << 16);
-}
 
 // Which prefix keys a work-group owns.
 struct Work {
@@ -133,6 +127,15 @@ __device__ inline float* partial_base(const AttnArgs& a, const Work& w, int D) {
 // ----------------------------------------------------------------------------
 // bf16 MFMA kernel
 // ----------------------------------------------------------------------------
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// Two floats -> two bf16 (round to nearest even) in one instruction.
+__device__ inline uint32_t pack2(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 template <int D>
 struct TileGeom {
   static constexpr int CH = D / 8;             // 16-byte chunks per key row
@@ -140,47 +143,115 @@ struct TileGeom {
   static constexpr int TILEB = kTile * ROWB;   // one tensor (K or V) of one tile
 };
 
-// Global -> registers for one 64-key tile: PER chunks of K and of V per thread.
-template <int D, int NT, bool PAGED>
-struct TileRegs {
-  static constexpr int PER = kTile * TileGeom<D>::CH / NT;
-  static_assert(PER >= 1, "tile too small for the work-group");
-  u32x4 k[PER], v[PER];
+constexpr int kMaxChunkPages = 512;            // page ids of one chunk staged in LDS
 
-  __device__ inline void load(const AttnArgs& a, const Work& w, int k0, bool is_new, int tid) {
-    constexpr int CH = TileGeom<D>::CH;
+// Streams 64-key K/V tiles of one work-group's chunk into registers.  A thread
+// owns chunks c = tid + i*NT of a tile: key rows row0 + i*RSTEP, elements
+// [e0, e0 + 8).  Full prefix tiles load unguarded from a per-tile base plus a
+// per-thread constant offset; the tail tile and the new-slot tile are guarded.
+template <int D, int NT, bool PAGED>
+struct KVStream {
+  static constexpr int CH = TileGeom<D>::CH;
+  static constexpr int PER = kTile * CH / NT;
+  static constexpr int RSTEP = NT / CH;
+  static_assert(PER >= 1 && NT % CH == 0, "tile too small for the work-group");
+
+  const char* kc;        // k_cache (bytes)
+  const char* vc;        // v_cache
+  int64_t seqoff;        // contiguous: sequence offset (bytes)
+  int64_t tokb, pageb;   // bytes per token / per page (paged)
+  int64_t toff;          // contiguous: (row0 * tok + kvh * head + e0) bytes; paged: (kvh * head + e0) bytes
+  int row0, e0, P;
+  bool lds_pages;        // page ids of this chunk are staged in s_pg
+  int pg_first;          // first page index of the chunk (in the sequence's block table)
+  const int32_t* bt;     // this sequence's block table row
+
+  __device__ inline void init(const AttnArgs& a, const Work& w, int tid, int* s_pg) {
+    row0 = tid / CH;
+    e0 = (tid % CH) * 8;
+    kc = static_cast<const char*>(a.k_cache);
+    vc = static_cast<const char*>(a.v_cache);
+    tokb = a.cs_tok * 2;
+    const int64_t hoff = (static_cast<int64_t>(w.kvh) * a.cs_head + e0) * 2;
+    if (PAGED) {
+      P = a.page_size;
+      pageb = a.cs_seq * 2;
+      toff = hoff;
+      bt = a.block_table + static_cast<int64_t>(w.b) * a.max_pages;
+      pg_first = w.kbeg / P;
+      const int npg = w.kend > w.kbeg ? (w.kend - 1) / P - pg_first + 1 : 0;
+      lds_pages = (kTile % P == 0) && npg <= kMaxChunkPages;
+      if (lds_pages)
+        for (int j = tid; j < npg; j += NT) s_pg[j] = bt[pg_first + j];
+    } else {
+      seqoff = static_cast<int64_t>(w.b) * a.cs_seq * 2;
+      toff = static_cast<int64_t>(row0) * tokb + hoff;
+    }
+  }
+
+  // Byte offset of this thread's chunk i of the prefix tile starting at key k0.
+  __device__ inline int64_t offset(int k0, int i, const int* s_pg) const {
+    const int row = row0 + i * RSTEP;
+    if (!PAGED) return seqoff + static_cast<int64_t>(k0 + i * RSTEP) * tokb + toff;
+    int64_t page;
+    int in_page;
+    if (lds_pages) {                          // P divides the tile: k0 % P == 0
+      page = s_pg[(k0 / P - pg_first) + row / P];
+      in_page = row % P;
+    } else {
+      const int key = k0 + row;
+      page = bt[key / P];
+      in_page = key % P;
+    }
+    return page * pageb + static_cast<int64_t>(in_page) * tokb + toff;
+  }
+
+  __device__ inline void load(u32x4 (&k)[PER], u32x4 (&v)[PER], const AttnArgs& a, const Work& w,
+                              int k0, bool is_new, const int* s_pg) const {
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    if (is_new) {
+      const char* kn = static_cast<const char*>(a.k_new);
+      const char* vn = static_cast<const char*>(a.v_new);
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * NT;
-      const int row = c / CH, e = (c % CH) * 8;
-      const u32x4 zero = {0u, 0u, 0u, 0u};
-      k[i] = zero;
-      v[i] = zero;
-      if (is_new) {
+      for (int i = 0; i < PER; ++i) {
+        const int row = row0 + i * RSTEP;
+        k[i] = zero;
+        v[i] = zero;
         if (row < a.n_new) {
-          const int64_t off = ((static_cast<int64_t>(w.b) * a.n_new + row) * a.hkv + w.kvh) * D + e;
-          k[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_new) + off);
-          v[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_new) + off);
+          const int64_t off = (((static_cast<int64_t>(w.b) * a.n_new + row) * a.hkv + w.kvh) * D + e0) * 2;
+          k[i] = *reinterpret_cast<const u32x4*>(kn + off);
+          v[i] = *reinterpret_cast<const u32x4*>(vn + off);
         }
-      } else {
-        const int key = k0 + row;
-        if (key < w.kend) {
-          const int64_t off = cache_offset<PAGED>(a, w.b, w.kvh, key, e);
-          k[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.k_cache) + off);
-          v[i] = *reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_cache) + off);
+      }
+    } else if (k0 + kTile <= w.kend) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int64_t off = offset(k0, i, s_pg);
+        k[i] = *reinterpret_cast<const u32x4*>(kc + off);
+        v[i] = *reinterpret_cast<const u32x4*>(vc + off);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        k[i] = zero;
+        v[i] = zero;
+        if (k0 + row0 + i * RSTEP < w.kend) {
+          const int64_t off = offset(k0, i, s_pg);
+          k[i] = *reinterpret_cast<const u32x4*>(kc + off);
+          v[i] = *reinterpret_cast<const u32x4*>(vc + off);
         }
       }
     }
   }
 
-  __device__ inline void store(uint8_t* sk, uint8_t* sv, int tid) const {
-    constexpr int CH = TileGeom<D>::CH, ROWB = TileGeom<D>::ROWB;
+  __device__ inline void store(uint8_t* sk, uint8_t* sv, const u32x4 (&k)[PER],
+                               const u32x4 (&v)[PER]) const {
+    constexpr int ROWB = TileGeom<D>::ROWB;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * NT;
-      const int row = c / CH, ch = c % CH;
-      *reinterpret_cast<u32x4*>(sk + row * ROWB + ch * 16) = k[i];
-      *reinterpret_cast<u32x4*>(sv + row * ROWB + ch * 16) = v[i];
+      const int off = (row0 + i * RSTEP) * ROWB + e0 * 2;
+      *reinterpret_cast<u32x4*>(sk + off) = k[i];
+      *reinterpret_cast<u32x4*>(sv + off) = v[i];
     }
   }
 };
@@ -193,28 +264,16 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   constexpr int ROWB = TileGeom<D>::ROWB;
   constexpr int TILEB = TileGeom<D>::TILEB;
   constexpr int PF = NW >= 8 ? 2 : 1;          // tiles prefetched into registers
+  using Stream = KVStream<D, NT, PAGED>;
+  constexpr int PER = Stream::PER;
   __shared__ __attribute__((aligned(16))) uint8_t smem[2][2][TILEB];   // [buffer][K, V]
   __shared__ uint64_t vis[kMaxNew];
+  __shared__ int s_pg[PAGED ? kMaxChunkPages : 1];
 
   Work w;
   if (!setup_work(a, w)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
-  const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
-  if (tid < kMaxNew)
-    vis[tid] = tid < a.n_new ? visibility_word(tid, step_row, w.gamma, a.B, a.n_new) : 0ull;
-
-  const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
-  const int nt = ntp + (w.split == 0 ? 1 : 0);
-  auto tile_k0 = [&](int it) { return w.kbeg + it * kTile; };
-
-  // Start streaming before anything else.
-  TileRegs<D, NT, PAGED> regs[PF];
-  regs[0].load(a, w, tile_k0(0), 0 == ntp, tid);
-  regs[0].store(smem[0][0], smem[0][1], tid);
-#pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (1 + p < nt) regs[(1 + p) % PF].load(a, w, tile_k0(1 + p), 1 + p == ntp, tid);
 
   const int rowl = wave * 32 + n;
   const int m = w.rb * a.rows_pb + rowl;
@@ -222,7 +281,8 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   const int t = row_in ? m / a.group : 0;
   const int hq = w.kvh * a.group + (row_in ? m % a.group : 0);
 
-  // Q^T operands of this lane's row: dims 16*ks + 8*h + [0, 8).
+  // Q^T operands of this lane's row (dims 16*ks + 8*h + [0, 8)), loaded first
+  // so that they have landed before the tile loop starts.
   bf16x8 qop[KS];
   {
     const bf16x8* qrow = reinterpret_cast<const bf16x8*>(
@@ -237,6 +297,24 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
       }
     }
   }
+  const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
+  if (tid < kMaxNew)
+    vis[tid] = tid < a.n_new ? visibility_word(tid, step_row, w.gamma, a.B, a.n_new) : 0ull;
+
+  Stream kv;
+  kv.init(a, w, tid, s_pg);
+  if (PAGED) __syncthreads();                  // staged page ids
+
+  const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
+  const int nt = ntp + (w.split == 0 ? 1 : 0);
+  auto tile_k0 = [&](int it) { return w.kbeg + it * kTile; };
+
+  u32x4 rk[PF][PER], rv[PF][PER];
+  kv.load(rk[0], rv[0], a, w, tile_k0(0), 0 == ntp, s_pg);
+  kv.store(smem[0][0], smem[0][1], rk[0], rv[0]);
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (1 + p < nt) kv.load(rk[(1 + p) % PF], rv[(1 + p) % PF], a, w, tile_k0(1 + p), 1 + p == ntp, s_pg);
   __syncthreads();
   const uint64_t myvis = row_in ? vis[t] : 0ull;
 
@@ -252,6 +330,7 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   // reads 4 dims at column 16*(g%2) + 4*q of key row 4*h + k.
   const int tr_row = 4 * h + ((lane & 15) >> 2);
   const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int k_rd = n * ROWB + 16 * h;          // K operand read offset within a 32-key block
 
   // The loop is unrolled by PF so that every register-set index is a
   // compile-time constant (a runtime index would put the sets in scratch).
@@ -265,17 +344,18 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
     const uint8_t* sk = smem[it & 1][0];
     const uint8_t* sv = smem[it & 1][1];
 
-    // S^T = K Q^T: two 32-key blocks.  Register j of block kb holds key
-    // 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
+    // S^T = K Q^T: two 32-key blocks, interleaved.  Register j of block kb
+    // holds key 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
     f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) s[kb][j] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ka =
-            *reinterpret_cast<const bf16x8*>(sk + (32 * kb + n) * ROWB + (16 * ks + 8 * h) * 2);
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sk + 32 * kb * ROWB + k_rd + 32 * ks);
         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s[kb], 0, 0, 0);
       }
     }
@@ -329,7 +409,7 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
       for (int hf = 0; hf < 2; ++hf) {
         u32x4 pw;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) pw[p] = pack_bf16x2(s[kb][8 * hf + 2 * p], s[kb][8 * hf + 2 * p + 1]);
+        for (int p = 0; p < 4; ++p) pw[p] = pack2(s[kb][8 * hf + 2 * p], s[kb][8 * hf + 2 * p + 1]);
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
         const uint8_t* vrow = sv + (32 * kb + 16 * hf + tr_row) * ROWB + tr_col * 2;
 #pragma unroll
@@ -346,9 +426,10 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
 
     // Next tile: registers -> the other LDS buffer, then refill the registers.
     if (it + 1 < nt) {
-      regs[(u + 1) % PF].store(smem[(it + 1) & 1][0], smem[(it + 1) & 1][1], tid);
+      const int nx = (u + 1) % PF;        // a constant once the u loop is unrolled
+      kv.store(smem[(it + 1) & 1][0], smem[(it + 1) & 1][1], rk[nx], rv[nx]);
       if (it + 1 + PF < nt)
-        regs[(u + 1) % PF].load(a, w, tile_k0(it + 1 + PF), it + 1 + PF == ntp, tid);
+        kv.load(rk[nx], rv[nx], a, w, tile_k0(it + 1 + PF), it + 1 + PF == ntp, s_pg);
     }
     __syncthreads();
   }
@@ -366,8 +447,8 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
     for (int c = 0; c < NB; ++c)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const u32x2 v = {pack_bf16x2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
-                         pack_bf16x2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
+        const u32x2 v = {pack2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
+                         pack2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
         *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * q + 4 * h) = v;
       }
     if (a.lse && h == 0)
@@ -565,7 +646,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   const float inv = ok ? 1.f / lsum : 0.f;
   const int64_t orow = ((static_cast<int64_t>(b) * a.n_new + t) * a.hq + hq) * D + d0;
   if constexpr (sizeof(OutT) == 2) {
-    const u32x2 pk = {pack_bf16x2(acc[0] * inv, acc[1] * inv), pack_bf16x2(acc[2] * inv, acc[3] * inv)};
+    const u32x2 pk = {pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
     *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.out) + orow) = pk;
   } else {
     *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = acc * inv;
