@@ -139,9 +139,21 @@ __device__ inline uint32_t pack2(float lo, float hi) {
 template <int D>
 struct TileGeom {
   static constexpr int CH = D / 8;             // 16-byte chunks per key row
-  static constexpr int ROWB = 2 * D + 32;      // LDS bytes per key row (padded)
+  static constexpr int ROWB = 2 * D;           // LDS bytes per key row (unpadded)
   static constexpr int TILEB = kTile * ROWB;   // one tensor (K or V) of one tile
 };
+
+// LDS swizzle: 16-byte chunk L of key row r is stored at chunk L ^ swz(r).  The
+// XOR masks were chosen (by exhaustive search over linear maps of r mod 16) so
+// that the K operand reads (32 rows, one chunk) and the transpose reads of V
+// (4 rows x 4 chunks per 32 lanes) hit distinct banks with 32 or 64 LDS banks.
+template <int D>
+__device__ inline int swz(int r) {
+  if constexpr (D == 128)
+    return ((r & 1) ? 4 : 0) ^ ((r & 2) ? 10 : 0) ^ ((r & 4) ? 1 : 0) ^ ((r & 8) ? 2 : 0);
+  else
+    return ((r & 1) ? 2 : 0) ^ ((r & 2) ? 4 : 0) ^ ((r & 4) ? 1 : 0) ^ ((r & 8) ? 2 : 0);
+}
 
 constexpr int kMaxChunkPages = 512;            // page ids of one chunk staged in LDS
 
@@ -249,15 +261,20 @@ struct KVStream {
     constexpr int ROWB = TileGeom<D>::ROWB;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int off = (row0 + i * RSTEP) * ROWB + e0 * 2;
+      const int row = row0 + i * RSTEP;
+      const int off = row * ROWB + 16 * ((e0 / 8) ^ swz<D>(row));
       *reinterpret_cast<u32x4*>(sk + off) = k[i];
       *reinterpret_cast<u32x4*>(sv + off) = v[i];
     }
   }
 };
 
-template <int D, int NW, bool PAGED>
-__global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
+// RW row waves of 32 rows each; KW = 2 pairs every row wave with a second wave
+// that takes the other 32-key half of each tile (small row blocks, where the
+// extra wave doubles the loads in flight); the two halves merge at the end.
+template <int D, int RW, int KW, bool PAGED>
+__global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
+  constexpr int NW = RW * KW;
   constexpr int NT = NW * 64;
   constexpr int NB = D / 32;                   // 32-dim output blocks
   constexpr int KS = D / 16;                   // k-steps of QK^T
@@ -274,8 +291,9 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   if (!setup_work(a, w)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
+  const int rw = wave % RW, kw = wave / RW;    // row wave, key half
 
-  const int rowl = wave * 32 + n;
+  const int rowl = rw * 32 + n;
   const int m = w.rb * a.rows_pb + rowl;
   const bool row_in = m < a.rows;
   const int t = row_in ? m / a.group : 0;
@@ -326,113 +344,138 @@ __global__ void __launch_bounds__(NW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   float m_run = kNegInf, l_run = 0.f;
   const float sl2 = a.scale_log2;
 
-  // Transpose-read addressing: lane (g = lane/16, k = (lane%16)/4, q = lane%4)
-  // reads 4 dims at column 16*(g%2) + 4*q of key row 4*h + k.
-  const int tr_row = 4 * h + ((lane & 15) >> 2);
-  const int tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int k_rd = n * ROWB + 16 * h;          // K operand read offset within a 32-key block
-
-  // The loop is unrolled by PF so that every register-set index is a
-  // compile-time constant (a runtime index would put the sets in scratch).
-  for (int it0 = 0; it0 < nt; it0 += PF) {
+  // Per-lane LDS read offsets (swizzled).  K operand of k-step ks: row n of a
+  // 32-key block, chunk 2*ks + h.  V transpose reads: lane (g = lane/16,
+  // k = (lane%16)/4, q = lane%4) reads 4 dims at column 32*c + 16*(g%2) + 4*q
+  // of key row 4*h + k (lo) or 8 + 4*h + k (hi) of a 16-key chunk.
+  int koff[KS], voff[NB][2];
 #pragma unroll
-  for (int u = 0; u < PF; ++u) {
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = n * ROWB + 16 * ((2 * ks + h) ^ swz<D>(n));
+  {
+    const int k = (lane & 15) >> 2, q = lane & 3, gg = (lane >> 4) & 1;
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int hl = 0; hl < 2; ++hl) {
+        const int r = 8 * hl + 4 * h + k;
+        const int L = 4 * c + 2 * gg + (q >> 1);
+        voff[c][hl] = r * ROWB + 16 * (L ^ swz<D>(r)) + 8 * (q & 1);
+      }
+  }
+
+  // The loop is unrolled by two: the LDS buffer and the register set are then
+  // compile-time indices (a runtime index would put the sets in scratch).
+  for (int it0 = 0; it0 < nt; it0 += 2) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
     const int it = it0 + u;
     if (it >= nt) break;
     const bool is_new = it == ntp;
     const int k0 = tile_k0(it);
-    const uint8_t* sk = smem[it & 1][0];
-    const uint8_t* sv = smem[it & 1][1];
+    const uint8_t* sk = smem[u][0];
+    const uint8_t* sv = smem[u][1];
 
-    // S^T = K Q^T: two 32-key blocks, interleaved.  Register j of block kb
-    // holds key 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
-    f32x16 s[2];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb0 = 0; kb0 < 2 / KW; ++kb0) {
+      const int kb = KW == 1 ? kb0 : kw;
+      // S^T = K Q^T for one 32-key block.  Register j holds key
+      // 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
+      f32x16 s;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) s[kb][j] = 0.f;
+      for (int j = 0; j < 16; ++j) s[j] = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sk + 32 * kb * ROWB + k_rd + 32 * ks);
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s[kb], 0, 0, 0);
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sk + 32 * kb * ROWB + koff[ks]);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s, 0, 0, 0);
       }
-    }
-    if (is_new) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      if (is_new) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int key = 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-          if (!((myvis >> key) & 1ull)) s[kb][j] = kNegInf;
+          if (!((myvis >> key) & 1ull)) s[j] = kNegInf;
         }
-    } else if (k0 + kTile > w.kend) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      } else if (k0 + kTile > w.kend) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
           const int key = k0 + 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-          if (key >= w.kend) s[kb][j] = kNegInf;
+          if (key >= w.kend) s[j] = kNegInf;
         }
-    }
+      }
 
-    float mx = kNegInf;
+      float mx = kNegInf;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float m_new = fmaxf(m_run, mx * sl2);
+      if (m_new > m_run + kLazy) {
+        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        l_run *= alpha;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[kb][j]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * sl2);
-    if (m_new > m_run + kLazy) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int c = 0; c < NB; ++c) o[c] *= alpha;
-      m_run = m_new;
-    }
-    const float moff = m_run == kNegInf ? 0.f : m_run;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+        for (int c = 0; c < NB; ++c) o[c] *= alpha;
+        m_run = m_new;
+      }
+      const float moff = m_run == kNegInf ? 0.f : m_run;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][j], sl2, -moff));
-        s[kb][j] = p;
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[j], sl2, -moff));
+        s[j] = p;
         l_run += p;
       }
 
-    // O^T += V^T P^T, one 16-key chunk at a time.  Chunk (kb, hf) covers keys
-    // 32*kb + 16*hf + kappa(h, i), kappa(h, i) = 8*(i/4) + 4*h + i%4.
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      // O^T += V^T P^T, two 16-key chunks.  Chunk hf covers keys
+      // 32*kb + 16*hf + kappa(h, i), kappa(h, i) = 8*(i/4) + 4*h + i%4.
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         u32x4 pw;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) pw[p] = pack2(s[kb][8 * hf + 2 * p], s[kb][8 * hf + 2 * p + 1]);
+        for (int p = 0; p < 4; ++p) pw[p] = pack2(s[8 * hf + 2 * p], s[8 * hf + 2 * p + 1]);
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-        const uint8_t* vrow = sv + (32 * kb + 16 * hf + tr_row) * ROWB + tr_col * 2;
+        const uint8_t* vblk = sv + (32 * kb + 16 * hf) * ROWB;
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (SIMSD_LDS s16x4*)(vrow + 64 * c));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (SIMSD_LDS s16x4*)(vrow + 8 * ROWB + 64 * c));
+          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SIMSD_LDS s16x4*)(vblk + voff[c][0]));
+          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SIMSD_LDS s16x4*)(vblk + voff[c][1]));
           const u32x2 l2 = __builtin_bit_cast(u32x2, lo), h2 = __builtin_bit_cast(u32x2, hi);
           const u32x4 vw = {l2[0], l2[1], h2[0], h2[1]};
           o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb, o[c], 0, 0, 0);
         }
       }
+    }
 
     // Next tile: registers -> the other LDS buffer, then refill the registers.
     if (it + 1 < nt) {
-      const int nx = (u + 1) % PF;        // a constant once the u loop is unrolled
-      kv.store(smem[(it + 1) & 1][0], smem[(it + 1) & 1][1], rk[nx], rv[nx]);
+      const int nx = (u + 1) % PF;         // a constant once the u loop is unrolled
+      kv.store(smem[1 - u][0], smem[1 - u][1], rk[nx], rv[nx]);
       if (it + 1 + PF < nt)
         kv.load(rk[nx], rv[nx], a, w, tile_k0(it + 1 + PF), it + 1 + PF == ntp, s_pg);
     }
     __syncthreads();
   }
+  }
+  if constexpr (KW == 2) {
+    // Merge the two key halves of each row through LDS (the tiles are free).
+    constexpr int SLOT = NB * 16 + 2;
+    float* xs = reinterpret_cast<float*>(&smem[0][0][0]) + (rw * 64 + lane) * SLOT;
+    if (kw == 1) {
+#pragma unroll
+      for (int c = 0; c < NB; ++c)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) xs[c * 16 + j] = o[c][j];
+      xs[NB * 16] = m_run;
+      xs[NB * 16 + 1] = l_run;
+    }
+    __syncthreads();
+    if (kw == 1) return;
+    const float m1 = xs[NB * 16], l1 = xs[NB * 16 + 1];
+    const float mm = fmaxf(m_run, m1);
+    const float mref = mm == kNegInf ? 0.f : mm;
+    const float a0 = __builtin_amdgcn_exp2f(m_run - mref), a1 = __builtin_amdgcn_exp2f(m1 - mref);
+#pragma unroll
+    for (int c = 0; c < NB; ++c)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) o[c][j] = o[c][j] * a0 + xs[c * 16 + j] * a1;
+    l_run = l_run * a0 + l1 * a1;
+    m_run = mm;
   }
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   if (!row_in) return;
@@ -657,12 +700,11 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 }
 
 template <int D, bool PAGED>
-void launch_bf16(int waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
-  switch (waves) {
-    case 1: hipLaunchKernelGGL((attn_bf16_kernel<D, 1, PAGED>), grid, dim3(64), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, PAGED>), grid, dim3(128), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, PAGED>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, PAGED>), grid, dim3(512), 0, st, a); break;
+void launch_bf16(int row_waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
+  switch (row_waves) {
+    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
   }
 }
 
@@ -680,11 +722,11 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const bool paged = d.page_size > 0;
   if (d.dtype == SIMSD_BF16) {
     if (d.head_dim == 128) {
-      if (paged) launch_bf16<128, true>(p.waves, grid, a, st);
-      else launch_bf16<128, false>(p.waves, grid, a, st);
+      if (paged) launch_bf16<128, true>(p.row_waves, grid, a, st);
+      else launch_bf16<128, false>(p.row_waves, grid, a, st);
     } else {
-      if (paged) launch_bf16<64, true>(p.waves, grid, a, st);
-      else launch_bf16<64, false>(p.waves, grid, a, st);
+      if (paged) launch_bf16<64, true>(p.row_waves, grid, a, st);
+      else launch_bf16<64, false>(p.row_waves, grid, a, st);
     }
   } else {
     if (d.head_dim == 128) launch_f32<128>(paged, grid, a, st);

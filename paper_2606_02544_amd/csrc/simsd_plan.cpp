@@ -65,13 +65,17 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   r.n_new = d->block_size + d->max_ref;
   r.rows = r.group * r.n_new;
   if (d->dtype == SIMSD_BF16) {
-    // One 32-row MFMA block per wave; power-of-two wave count, at most 8.
+    // One 32-row MFMA block per row wave; a power of two in [2, 8].  With two
+    // row waves, each is paired with a second wave taking the other half of
+    // every key tile.
     const int need = static_cast<int>(ceil_div(std::min(r.rows, 256), 32));
-    r.waves = 1;
-    while (r.waves < need) r.waves *= 2;
-    r.rows_pb = r.waves * 32;
+    r.row_waves = 2;
+    while (r.row_waves < need) r.row_waves *= 2;
+    r.waves = r.row_waves == 2 ? 4 : r.row_waves;
+    r.rows_pb = r.row_waves * 32;
   } else {
     r.waves = 4;          // 8 rows per wave, one wave per row at a time
+    r.row_waves = 4;
     r.rows_pb = 32;
   }
   r.row_blocks = static_cast<int>(ceil_div(r.rows, r.rows_pb));

@@ -24,6 +24,7 @@ struct AttnPlan {
   int n_new = 0;        // B + L
   int rows = 0;         // M = group * n_new packed query rows per (sequence, KV head)
   int waves = 0;        // waves per work-group
+  int row_waves = 0;    // waves that own distinct rows (bf16: 32 rows each)
   int rows_pb = 0;      // rows per work-group (row block)
   int row_blocks = 0;   // ceil(rows / rows_pb)
   int chunk = 0;        // prefix keys per split
