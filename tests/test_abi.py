@@ -20,6 +20,15 @@ HEADER = os.path.join(ROOT, "include", "simsd.h")
 FAKE = ctypes.c_void_p(0x10000)     # aligned, never dereferenced
 
 
+def _no_gpu():
+    """The fake-pointer calls below must fail host validation; as a second
+    guard they only run where no GPU is visible, so a validation bug can never
+    launch a kernel on bogus pointers."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("host-validation tests run only without a visible GPU")
+
+
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -78,6 +87,7 @@ def test_workspace_sizes_follow_the_plan():
 
 
 def call_attention(desc, **over):
+    _no_gpu()
     args = dict(q=FAKE, k_new=FAKE, v_new=FAKE, k_cache=FAKE, v_cache=FAKE, block_table=FAKE,
                 prefix_lens=FAKE, step_map=FAKE, num_ref=FAKE, out=FAKE, lse=None,
                 workspace=None, ws_bytes=0)
@@ -110,7 +120,7 @@ def test_attention_descriptor_errors(field, value, status):
 
 
 def test_attention_pointer_alignment_and_workspace_errors():
-    desc = cfg_desc(2)
+    desc = cfg_desc(2, kv_chunk=64)          # needs a workspace
     ws = binding.attention_workspace_size(desc)
     assert call_attention(desc, q=None, workspace=FAKE, ws_bytes=ws)[0] == 1
     assert call_attention(desc, k_cache=None, workspace=FAKE, ws_bytes=ws)[0] == 1
@@ -126,6 +136,7 @@ def test_attention_pointer_alignment_and_workspace_errors():
 
 
 def call_accept(desc, **over):
+    _no_gpu()
     a = dict(logits=FAKE, draft_ids=FAKE, step_map=FAKE, num_ref=FAKE, target_ids=FAKE,
              confidence=None, draft_prob=None, accept_len=FAKE, workspace=FAKE, ws=1 << 30)
     a.update(over)
