@@ -7,8 +7,10 @@
 // lane, the running maximum, the first vector reaching it and the sum of
 // exp(x - max).  Partials are merged in (value desc, index asc) order, so ties
 // resolve to the lowest vocabulary index exactly.  A second kernel, one
-// work-group per sequence, merges the chunks of all its rows, computes
-// confidence and draft probabilities and walks the drafts in step order.
+// work-group per sequence, issues its loads in two rounds (step map, drafts
+// and every chunk partial of its rows; then the drafted tokens' logits),
+// merges the chunks, computes confidence and draft probabilities and finds the
+// accepted prefix with one wave ballot.
 #include "simsd_kernels.h"
 
 namespace simsd {
@@ -166,55 +168,163 @@ __global__ void __launch_bounds__(NT) scan_kernel(AcceptArgs a) {
   }
 }
 
+// Partials a wave keeps in registers when it loads all its rows at once.
+constexpr int kFinalRegs = 16;
+
+// Loads the chunk partials of this wave's rows (wave, wave + NWV, ...), PPL
+// per lane per row, all before the first wait; returns them in registers.
+template <int PPL>
+__device__ inline void load_rows(const AcceptArgs& a, const AcceptPartial* pb, int wave, int lane,
+                                 AcceptPartial (&buf)[kFinalRegs]) {
+  constexpr int NWV = NT / 64;
+  // Indices are clamped so that every load is unconditional and in bounds
+  // (a guarded load would make the compiler wait on it right away); the merge
+  // ignores the duplicates.
+#pragma unroll
+  for (int i = 0; i < kFinalRegs; ++i) {
+    const int kk = min(wave + NWV * (i / PPL), a.B - 1), cc = min(lane + 64 * (i % PPL), a.cpr - 1);
+    buf[i] = pb[static_cast<int64_t>(kk) * a.cpr + cc];
+  }
+}
+
+// cpr <= 64: the wave's rows are packed 64 / P2 to a register (P2 = cpr
+// rounded up to a power of two, lg = log2 P2), so one log2(P2)-step
+// reduction merges them all.
+__device__ inline void load_packed(const AcceptArgs& a, const AcceptPartial* pb, int wave, int lane,
+                                   int lg, AcceptPartial (&buf)[kFinalRegs]) {
+  constexpr int NWV = NT / 64;
+  const int R = 64 >> lg;
+#pragma unroll
+  for (int p = 0; p < kFinalRegs; ++p) {
+    const int kk = min(wave + NWV * (p * R + (lane >> lg)), a.B - 1);
+    const int cc = min(lane & ((1 << lg) - 1), a.cpr - 1);
+    buf[p] = pb[static_cast<int64_t>(kk) * a.cpr + cc];
+  }
+}
+
+__device__ inline void merge_packed(const AcceptArgs& a, int wave, int lane, int lg, int rpw,
+                                    const AcceptPartial (&buf)[kFinalRegs], Best* s_row) {
+  constexpr int NWV = NT / 64;
+  const int R = 64 >> lg;
+#pragma unroll
+  for (int p = 0; p < kFinalRegs; ++p) {
+    if (p * R >= rpw) break;
+    const int kk = wave + NWV * (p * R + (lane >> lg));
+    const int cc = lane & ((1 << lg) - 1);
+    Best r = {kNegInf, kNoIndex, 0.f};
+    if (cc < a.cpr && kk < a.B) r = Best{buf[p].mx, buf[p].ix, buf[p].sm};
+    for (int sh = (1 << lg) >> 1; sh >= 1; sh >>= 1) {
+      Best o;
+      o.mx = __shfl_xor(r.mx, sh);
+      o.ix = __shfl_xor(r.ix, sh);
+      o.sm = __shfl_xor(r.sm, sh);
+      r = combine(r, o);
+    }
+    if (cc == 0 && kk < a.B) s_row[kk] = r;
+  }
+}
+
+template <int PPL>
+__device__ inline void merge_rows(const AcceptArgs& a, int wave, int lane,
+                                  const AcceptPartial (&buf)[kFinalRegs], Best* s_row) {
+  constexpr int NWV = NT / 64;
+#pragma unroll
+  for (int j = 0; j < kFinalRegs / PPL; ++j) {
+    const int kk = wave + NWV * j;
+    if (kk >= a.B) break;
+    Best r = {kNegInf, kNoIndex, 0.f};
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      const AcceptPartial pr = buf[j * PPL + q];
+      if (lane + 64 * q < a.cpr) r = combine(r, Best{pr.mx, pr.ix, pr.sm});
+    }
+    r = wave_reduce(r);
+    if (lane == 0) s_row[kk] = r;
+  }
+}
+
 // One work-group per sequence: merge the chunks of every row, then the
 // per-row outputs, draft probabilities and the accepted-prefix length.
 template <bool BF16>
 __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
+  constexpr int NWV = NT / 64;
   __shared__ Best s_row[kMaxNew];
+  __shared__ int s_step[kMaxNew];
   __shared__ int s_row_of_step[kMaxNew];
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(b) * a.B;
+  const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.B * a.cpr;
   const int esz = BF16 ? 2 : 4;
   const char* logits_b = static_cast<const char*>(a.logits) + static_cast<int64_t>(b) * a.B * a.V * esz;
-  const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.B * a.cpr;
-  for (int kk = wave; kk < a.B; kk += NT / 64) {
-    Best r = {kNegInf, kNoIndex, 0.f};
-    if (step_row[kk] >= 1) {
+
+  // First round of loads, none waiting on another: step map, this lane's
+  // draft, and the chunk partials of every row (rows that were not scanned
+  // hold stale partials, which are never used).
+  // A zero the compiler cannot see through keeps this a vector load issued
+  // with the others (as a scalar load it is scheduled after the first wait).
+  int lane_zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(lane_zero));
+  const int nref = a.num_ref[b + lane_zero];
+  const int step_t = step_row[min(tid, a.B - 1)];
+  int tok = -1;
+  if (a.L > 0) tok = a.draft_ids[static_cast<int64_t>(b) * a.L + min(lane, a.L - 1)];
+  const int rpw = (a.B + NWV - 1) / NWV;     // rows of this wave: wave, wave + NWV, ...
+  const int ppl = (a.cpr + 63) / 64;         // partials per lane per row
+  const int mode = ppl == 1 && rpw <= kFinalRegs ? 1 : ppl == 2 && 2 * rpw <= kFinalRegs ? 2
+                 : ppl <= 4 && 4 * rpw <= kFinalRegs ? 4 : 0;
+  const int lg = 32 - __clz(max(a.cpr, 1) - 1);   // ceil(log2(cpr)), <= 6 in mode 1
+  AcceptPartial buf[kFinalRegs];
+  if (mode == 1) load_packed(a, pb, wave, lane, lg, buf);
+  else if (mode == 2) load_rows<2>(a, pb, wave, lane, buf);
+  else if (mode == 4) load_rows<4>(a, pb, wave, lane, buf);
+  if (tid < a.B) s_step[tid] = step_t;
+  if (tid < kMaxNew) s_row_of_step[tid] = -1;
+  const int gamma = min(max(nref, 0), a.L);
+  __syncthreads();
+  if (tid < a.B && step_t >= 1 && step_t <= gamma) s_row_of_step[step_t - 1] = tid;
+  __syncthreads();
+
+  // Second round: the drafted token's logit at its verification row.
+  const int r = lane;
+  int kr = -1;
+  float x = 0.f;
+  if (wave == 0 && r < gamma) {
+    kr = s_row_of_step[r];
+    if (kr >= 0 && tok >= 0 && tok < a.V)
+      x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
+  }
+
+  if (mode == 1) merge_packed(a, wave, lane, lg, rpw, buf, s_row);
+  else if (mode == 2) merge_rows<2>(a, wave, lane, buf, s_row);
+  else if (mode == 4) merge_rows<4>(a, wave, lane, buf, s_row);
+  else {
+    for (int kk = wave; kk < a.B; kk += NWV) {
+      Best rr = {kNegInf, kNoIndex, 0.f};
       for (int cc = lane; cc < a.cpr; cc += 64) {
         const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
-        r = combine(r, Best{pr.mx, pr.ix, pr.sm});
+        rr = combine(rr, Best{pr.mx, pr.ix, pr.sm});
       }
-      r = wave_reduce(r);
+      rr = wave_reduce(rr);
+      if (lane == 0) s_row[kk] = rr;
     }
-    if (lane == 0) s_row[kk] = r;
   }
-  const int gamma = min(max(a.num_ref[b], 0), a.L);
-  if (tid < kMaxNew) s_row_of_step[tid] = -1;
   __syncthreads();
   if (tid < a.B) {
-    const int s = step_row[tid];
-    if (s >= 1 && s <= gamma) s_row_of_step[s - 1] = tid;
-    const bool scanned = s >= 1;
+    const bool scanned = s_step[tid] >= 1;
     a.target_ids[static_cast<int64_t>(b) * a.B + tid] = scanned ? s_row[tid].ix : -1;
     if (a.confidence)
       a.confidence[static_cast<int64_t>(b) * a.B + tid] = scanned ? 1.f / s_row[tid].sm : 0.f;
   }
-  __syncthreads();
-  // One lane per draft r: its verification row, match flag and probability.
-  // The accepted prefix ends at the first rejected draft (a wave ballot).
+  // One lane per draft r: match flag and probability; the accepted prefix
+  // ends at the first rejected draft (a wave ballot).
   if (wave == 0) {
-    const int r = lane;
     bool rejected = false;
     float p = 0.f;
     if (r < gamma) {
-      const int kr = s_row_of_step[r];
-      const int tok = a.draft_ids[static_cast<int64_t>(b) * a.L + r];
       rejected = kr < 0 || s_row[kr].ix != tok;
-      if (kr >= 0 && tok >= 0 && tok < a.V) {
-        const float x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
+      if (kr >= 0 && tok >= 0 && tok < a.V)
         p = __builtin_amdgcn_exp2f((x - s_row[kr].mx) * kLog2e) / s_row[kr].sm;
-      }
     }
     if (a.draft_prob && r < a.L) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = p;
     const unsigned long long rej = __ballot(rejected);

@@ -15,9 +15,10 @@
 // max and sum, and a second kernel merges them; there is no device-wide fence
 // or counter in the streaming kernel.
 //
-// bf16 path: K and V tiles of 64 keys are loaded into registers one tile ahead
-// (two ahead for 8-wave groups) and written to a double-buffered LDS ring with
-// 288-byte rows (no bank conflicts for the reads below).  Scores are computed
+// bf16 path: K and V tiles of 64 keys stream into a ring of LDS tile slots
+// with direct global->LDS loads issued up to three tiles ahead, so no
+// registers hold data in flight; rows are XOR-swizzled in 16-byte chunks so
+// that the reads below are free of bank conflicts.  Scores are computed
 // transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16, so lane l owns query
 // row l % 32 of its wave's 32-row block and a row's softmax state stays in two
 // lanes (l, l ^ 32).  O^T = V^T P^T takes P straight from the score registers
@@ -52,38 +53,41 @@ struct SlotLabel {
   int tau;
 };
 
-__device__ inline SlotLabel slot_label(int slot, const int32_t* step_row, int gamma, int B) {
+// Label of new slot `slot` given its block-slot step (ignored for reference
+// slots).
+__device__ inline SlotLabel slot_label(int slot, int step, int gamma, int B) {
   if (slot < B) {
-    const int s = step_row[slot];
-    if (s < 0) return {-1, -1};
-    return {0, s > gamma ? gamma + 1 : s};
+    if (step < 0) return {-1, -1};
+    return {0, step > gamma ? gamma + 1 : step};
   }
   const int r = slot - B;
   if (r >= gamma) return {-1, -1};
   return {1, r + 1};
 }
 
-// Bit j is set iff new row i may attend to new slot j.  Zero for padding rows.
-__device__ uint64_t visibility_word(int i, const int32_t* step_row, int gamma, int B, int n_new) {
-  const SlotLabel li = slot_label(i, step_row, gamma, B);
-  if (li.sec < 0) return 0ull;
-  uint64_t w = 0ull;
-  for (int j = 0; j < n_new; ++j) {
-    const SlotLabel lj = slot_label(j, step_row, gamma, B);
-    bool v;
-    if (lj.sec < 0)
-      v = false;
-    else if (lj.sec == 0 && lj.tau == 0)
-      v = true;
-    else if (li.sec == 1)
-      v = (lj.sec == 1) ? (lj.tau <= li.tau) : (lj.tau > li.tau);
-    else
-      v = (lj.sec == 1) ? (lj.tau < li.tau) : (lj.tau >= li.tau);
-    w |= static_cast<uint64_t>(v) << j;
-  }
-  return w;
+// Whether a non-padded row with label li may attend to new slot lj.
+__device__ inline bool slot_visible(SlotLabel li, SlotLabel lj) {
+  if (lj.sec < 0) return false;
+  if (lj.sec == 0 && lj.tau == 0) return true;
+  if (li.sec == 1) return lj.sec == 1 ? lj.tau <= li.tau : lj.tau > li.tau;
+  return lj.sec == 1 ? lj.tau < li.tau : lj.tau >= li.tau;
 }
 
+// Visibility words of the new slots, one 64-bit word per row (bit j: the row
+// may attend to slot j; zero for padding rows), written to vis[0, n_new).
+// Lane j holds slot j's label; row i's word is one ballot against the label
+// of lane i.  `step` is lane j's block-slot step (any value for j >= B).
+template <int NW>
+__device__ inline void build_visibility(uint64_t* vis, int step, int gamma, int B, int n_new,
+                                        int wave, int lane) {
+  const SlotLabel lj = slot_label(lane, step, gamma, B);
+  for (int i = wave; i < n_new; i += NW) {
+    const SlotLabel li = {__builtin_amdgcn_readlane(lj.sec, i), __builtin_amdgcn_readlane(lj.tau, i)};
+    const bool v = lane < n_new && li.sec >= 0 && slot_visible(li, lj);
+    const uint64_t word = __ballot(v);
+    if (lane == 0) vis[i] = word;
+  }
+}
 
 // Which prefix keys a work-group owns.
 struct Work {
@@ -136,6 +140,18 @@ __device__ inline uint32_t pack2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
+// Combine a value across lanes l and l ^ 32 (the two halves of an MFMA
+// column) with one VALU lane swap instead of an LDS permute.  Both halves
+// get the same bits (low half's value first).
+__device__ inline float xhalf_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float xhalf_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int D>
 struct TileGeom {
   static constexpr int CH = D / 8;             // 16-byte chunks per key row
@@ -157,133 +173,149 @@ __device__ inline int swz(int r) {
 
 constexpr int kMaxChunkPages = 512;            // page ids of one chunk staged in LDS
 
-// Streams 64-key K/V tiles of one work-group's chunk into registers.  A thread
-// owns chunks c = tid + i*NT of a tile: key rows row0 + i*RSTEP, elements
-// [e0, e0 + 8).  Full prefix tiles load unguarded from a per-tile base plus a
-// per-thread constant offset; the tail tile and the new-slot tile are guarded.
-template <int D, int NT, bool PAGED>
-struct KVStream {
-  static constexpr int CH = TileGeom<D>::CH;
-  static constexpr int PER = kTile * CH / NT;
-  static constexpr int RSTEP = NT / CH;
-  static_assert(PER >= 1 && NT % CH == 0, "tile too small for the work-group");
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane i's bytes land at LDS byte lds + 16 * i, so one instruction moves 1 KB.
+// It counts in vmcnt like any vector load but the compiler does not track it:
+// readers wait with wait_vm and then pass a barrier.  M0 (the LDS base) is a
+// reserved register that the compiler does not allocate to values, so setting
+// it here disturbs nothing.
+__device__ inline void dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+// This wave's LDS accesses complete, then a work-group barrier.  Unlike
+// __syncthreads it does not wait for vector memory, so tiles still loading
+// stay in flight.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-  const char* kc;        // k_cache (bytes)
-  const char* vc;        // v_cache
-  int64_t seqoff;        // contiguous: sequence offset (bytes)
-  int64_t tokb, pageb;   // bytes per token / per page (paged)
-  int64_t toff;          // contiguous: (row0 * tok + kvh * head + e0) bytes; paged: (kvh * head + e0) bytes
-  int row0, e0, P;
-  bool lds_pages;        // page ids of this chunk are staged in s_pg
-  int pg_first;          // first page index of the chunk (in the sequence's block table)
-  const int32_t* bt;     // this sequence's block table row
+// Streams 64-key K/V tiles of one work-group's chunk into a ring of LDS tile
+// slots with direct loads.  One instruction covers RPI key rows of one
+// tensor; lane i writes chunk position i % CPR of row i / CPR of its block
+// and so fetches logical chunk (i % CPR) ^ swz(row).  The tiles are split
+// between the waves by instruction.  Rows past the prefix (the tail tile) or
+// past the new slots (the new-slot tile) read the last valid row instead:
+// their scores are masked and their values are finite, so they add zeros.
+template <int D, int NW, bool PAGED>
+struct KVRing {
+  static constexpr int ROWB = TileGeom<D>::ROWB, TILEB = TileGeom<D>::TILEB;
+  static constexpr int CPR = D / 8;            // 16-byte chunks per key row
+  static constexpr int RPI = 1024 / ROWB;      // key rows per instruction
+  static constexpr int IPT = kTile / RPI;      // instructions per tensor per tile
+  static constexpr int PERW = 2 * IPT / NW;    // instructions per wave per tile
+  static_assert(PERW >= 1 && (2 * IPT) % NW == 0, "tile instructions split evenly over the waves");
+
+  const char* kc;
+  const char* vc;
+  const char* kn;
+  const char* vn;
+  int64_t seqoff;         // contiguous: this sequence's cache offset (bytes)
+  int64_t tokb, pageb;    // bytes per token, per page
+  int64_t hoff;           // this KV head (bytes)
+  int64_t newoff, newrow; // new slots: offset of slot 0 of (sequence, KV head), bytes per slot
+  int64_t loff[PERW];     // full tiles: per-instruction lane offset (bytes)
+  int pgrel[PERW];        // paged full tiles: page of the row relative to the tile's first
+  int row[PERW], chunk[PERW];
+  int wave, P, pg_first, n_new;
+  bool lds_pages;         // page ids of this chunk are staged in s_pg
+  const int32_t* bt;      // this sequence's block table row
 
   __device__ inline void init(const AttnArgs& a, const Work& w, int tid, int* s_pg) {
-    row0 = tid / CH;
-    e0 = (tid % CH) * 8;
+    wave = tid >> 6;
+    const int lane = tid & 63;
     kc = static_cast<const char*>(a.k_cache);
     vc = static_cast<const char*>(a.v_cache);
+    kn = static_cast<const char*>(a.k_new);
+    vn = static_cast<const char*>(a.v_new);
     tokb = a.cs_tok * 2;
-    const int64_t hoff = (static_cast<int64_t>(w.kvh) * a.cs_head + e0) * 2;
+    hoff = static_cast<int64_t>(w.kvh) * a.cs_head * 2;
+    n_new = a.n_new;
+    newrow = static_cast<int64_t>(a.hkv) * D * 2;
+    newoff = (static_cast<int64_t>(w.b) * a.n_new * a.hkv + w.kvh) * D * 2;
     if (PAGED) {
       P = a.page_size;
       pageb = a.cs_seq * 2;
-      toff = hoff;
       bt = a.block_table + static_cast<int64_t>(w.b) * a.max_pages;
       pg_first = w.kbeg / P;
       const int npg = w.kend > w.kbeg ? (w.kend - 1) / P - pg_first + 1 : 0;
       lds_pages = (kTile % P == 0) && npg <= kMaxChunkPages;
       if (lds_pages)
-        for (int j = tid; j < npg; j += NT) s_pg[j] = bt[pg_first + j];
+        for (int j = tid; j < npg; j += NW * 64) s_pg[j] = bt[pg_first + j];
     } else {
       seqoff = static_cast<int64_t>(w.b) * a.cs_seq * 2;
-      toff = static_cast<int64_t>(row0) * tokb + hoff;
+    }
+#pragma unroll
+    for (int i = 0; i < PERW; ++i) {
+      const int g = wave * PERW + i;
+      row[i] = (g % IPT) * RPI + lane / CPR;
+      chunk[i] = (lane % CPR) ^ swz<D>(row[i]);
+      if (PAGED) {
+        pgrel[i] = lds_pages ? row[i] / P : 0;
+        loff[i] = static_cast<int64_t>(lds_pages ? row[i] % P : 0) * tokb + hoff + chunk[i] * 16;
+      } else {
+        loff[i] = static_cast<int64_t>(row[i]) * tokb + hoff + chunk[i] * 16;
+      }
     }
   }
 
-  // Byte offset of this thread's chunk i of the prefix tile starting at key k0.
-  __device__ inline int64_t offset(int k0, int i, const int* s_pg) const {
-    const int row = row0 + i * RSTEP;
-    if (!PAGED) return seqoff + static_cast<int64_t>(k0 + i * RSTEP) * tokb + toff;
-    int64_t page;
-    int in_page;
-    if (lds_pages) {                          // P divides the tile: k0 % P == 0
-      page = s_pg[(k0 / P - pg_first) + row / P];
-      in_page = row % P;
-    } else {
-      const int key = k0 + row;
-      page = bt[key / P];
-      in_page = key % P;
-    }
-    return page * pageb + static_cast<int64_t>(in_page) * tokb + toff;
+  // Byte offset of (key, this head, element 0) in the cache (general path).
+  __device__ inline int64_t key_offset(int key, const int* s_pg) const {
+    if (!PAGED) return seqoff + static_cast<int64_t>(key) * tokb + hoff;
+    const int64_t page = lds_pages ? s_pg[key / P - pg_first] : bt[key / P];
+    return page * pageb + static_cast<int64_t>(key % P) * tokb + hoff;
   }
 
-  __device__ inline void load(u32x4 (&k)[PER], u32x4 (&v)[PER], const AttnArgs& a, const Work& w,
-                              int k0, bool is_new, const int* s_pg) const {
-    const u32x4 zero = {0u, 0u, 0u, 0u};
+  // Issue this wave's share of the tile starting at prefix key k0 (or of the
+  // new-slot tile) into the ring slot at LDS byte address `slot`.
+  __device__ inline void issue(uint32_t slot, int k0, bool is_new, int kend, const int* s_pg) const {
     if (is_new) {
-      const char* kn = static_cast<const char*>(a.k_new);
-      const char* vn = static_cast<const char*>(a.v_new);
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int row = row0 + i * RSTEP;
-        k[i] = zero;
-        v[i] = zero;
-        if (row < a.n_new) {
-          const int64_t off = (((static_cast<int64_t>(w.b) * a.n_new + row) * a.hkv + w.kvh) * D + e0) * 2;
-          k[i] = *reinterpret_cast<const u32x4*>(kn + off);
-          v[i] = *reinterpret_cast<const u32x4*>(vn + off);
-        }
+      for (int i = 0; i < PERW; ++i) {
+        const int g = wave * PERW + i;
+        const int r = min(row[i], n_new - 1);
+        const char* src = (g < IPT ? kn : vn) + newoff + r * newrow + chunk[i] * 16;
+        dma16(src, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
-    } else if (k0 + kTile <= w.kend) {
+    } else if (k0 + kTile <= kend && (!PAGED || lds_pages)) {
+      int64_t tbase = 0;
+      int pbase = 0;
+      if (PAGED) pbase = k0 / P - pg_first;
+      else tbase = seqoff + static_cast<int64_t>(k0) * tokb;
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        const int64_t off = offset(k0, i, s_pg);
-        k[i] = *reinterpret_cast<const u32x4*>(kc + off);
-        v[i] = *reinterpret_cast<const u32x4*>(vc + off);
+      for (int i = 0; i < PERW; ++i) {
+        const int g = wave * PERW + i;
+        const int64_t off = PAGED ? static_cast<int64_t>(s_pg[pbase + pgrel[i]]) * pageb + loff[i]
+                                  : tbase + loff[i];
+        dma16((g < IPT ? kc : vc) + off, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
     } else {
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        k[i] = zero;
-        v[i] = zero;
-        if (k0 + row0 + i * RSTEP < w.kend) {
-          const int64_t off = offset(k0, i, s_pg);
-          k[i] = *reinterpret_cast<const u32x4*>(kc + off);
-          v[i] = *reinterpret_cast<const u32x4*>(vc + off);
-        }
+      for (int i = 0; i < PERW; ++i) {
+        const int g = wave * PERW + i;
+        const int key = min(k0 + row[i], kend - 1);
+        const int64_t off = key_offset(key, s_pg) + chunk[i] * 16;
+        dma16((g < IPT ? kc : vc) + off, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
-    }
-  }
-
-  __device__ inline void store(uint8_t* sk, uint8_t* sv, const u32x4 (&k)[PER],
-                               const u32x4 (&v)[PER]) const {
-    constexpr int ROWB = TileGeom<D>::ROWB;
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int row = row0 + i * RSTEP;
-      const int off = row * ROWB + 16 * ((e0 / 8) ^ swz<D>(row));
-      *reinterpret_cast<u32x4*>(sk + off) = k[i];
-      *reinterpret_cast<u32x4*>(sv + off) = v[i];
     }
   }
 };
 
 // RW row waves of 32 rows each; KW = 2 pairs every row wave with a second wave
 // that takes the other 32-key half of each tile (small row blocks, where the
-// extra wave doubles the loads in flight); the two halves merge at the end.
-template <int D, int RW, int KW, bool PAGED>
+// extra wave doubles the work in flight); the two halves merge at the end.
+// NBUF tiles of the ring: tile it + NBUF - 1 loads while tile it is read.
+template <int D, int RW, int KW, int NBUF, bool PAGED>
 __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   constexpr int NW = RW * KW;
-  constexpr int NT = NW * 64;
   constexpr int NB = D / 32;                   // 32-dim output blocks
   constexpr int KS = D / 16;                   // k-steps of QK^T
   constexpr int ROWB = TileGeom<D>::ROWB;
   constexpr int TILEB = TileGeom<D>::TILEB;
-  constexpr int PF = NW >= 8 ? 2 : 1;          // tiles prefetched into registers
-  using Stream = KVStream<D, NT, PAGED>;
-  constexpr int PER = Stream::PER;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2][2][TILEB];   // [buffer][K, V]
+  using Ring = KVRing<D, NW, PAGED>;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF][2][TILEB];   // [slot][K, V]
   __shared__ uint64_t vis[kMaxNew];
   __shared__ int s_pg[PAGED ? kMaxChunkPages : 1];
 
@@ -292,6 +324,10 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int n = lane & 31, h = lane >> 5;
   const int rw = wave % RW, kw = wave / RW;    // row wave, key half
+
+  // This lane's block-slot step (slot = lane), for the visibility words.
+  const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
+  const int lane_step = step_row[min(lane, a.B - 1)];
 
   const int rowl = rw * 32 + n;
   const int m = w.rb * a.rows_pb + rowl;
@@ -315,25 +351,22 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       }
     }
   }
-  const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
-  if (tid < kMaxNew)
-    vis[tid] = tid < a.n_new ? visibility_word(tid, step_row, w.gamma, a.B, a.n_new) : 0ull;
-
-  Stream kv;
+  Ring kv;
   kv.init(a, w, tid, s_pg);
   if (PAGED) __syncthreads();                  // staged page ids
 
   const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
   const int nt = ntp + (w.split == 0 ? 1 : 0);
   auto tile_k0 = [&](int it) { return w.kbeg + it * kTile; };
-
-  u32x4 rk[PF][PER], rv[PF][PER];
-  kv.load(rk[0], rv[0], a, w, tile_k0(0), 0 == ntp, s_pg);
-  kv.store(smem[0][0], smem[0][1], rk[0], rv[0]);
+  const uint32_t ring0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (SIMSD_LDS void*)(&smem[0][0][0])));      // LDS byte address of slot 0
+  constexpr uint32_t kSlotBytes = 2 * TILEB;
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (1 + p < nt) kv.load(rk[(1 + p) % PF], rv[(1 + p) % PF], a, w, tile_k0(1 + p), 1 + p == ntp, s_pg);
-  __syncthreads();
+  for (int j = 0; j < NBUF - 1; ++j)
+    if (j < nt) kv.issue(ring0 + j * kSlotBytes, tile_k0(j), j == ntp, w.kend, s_pg);
+
+  build_visibility<NW>(vis, lane_step, w.gamma, a.B, a.n_new, wave, lane);
+  __syncthreads();                             // visibility words; every load above has landed
   const uint64_t myvis = row_in ? vis[t] : 0ull;
 
   f32x16 o[NB];
@@ -363,15 +396,25 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       }
   }
 
-  // The loop is unrolled by two: the LDS buffer and the register set are then
-  // compile-time indices (a runtime index would put the sets in scratch).
-  for (int it0 = 0; it0 < nt; it0 += 2) {
+  // The loop is unrolled by NBUF so that ring slots are compile-time offsets.
+  for (int it0 = 0; it0 < nt; it0 += NBUF) {
 #pragma unroll
-  for (int u = 0; u < 2; ++u) {
+  for (int u = 0; u < NBUF; ++u) {
     const int it = it0 + u;
     if (it >= nt) break;
     const bool is_new = it == ntp;
     const int k0 = tile_k0(it);
+    // This wave's share of tile `it` has landed once at most the loads of the
+    // younger tiles remain (vector memory completes in issue order).
+    const int younger = min(nt - 1, it + NBUF - 2) - it;
+    if (NBUF >= 4 && younger >= 2) wait_vm<2 * Ring::PERW>();
+    else if (NBUF >= 3 && younger >= 1) wait_vm<Ring::PERW>();
+    else wait_vm<0>();
+    lds_barrier();                             // all of tile `it` is in; slot of tile it-1 is free
+    if (it + NBUF - 1 < nt) {
+      const int nx = it + NBUF - 1;
+      kv.issue(ring0 + ((u + NBUF - 1) % NBUF) * kSlotBytes, tile_k0(nx), nx == ntp, w.kend, s_pg);
+    }
     const uint8_t* sk = smem[u][0];
     const uint8_t* sv = smem[u][1];
 
@@ -405,7 +448,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       float mx = kNegInf;
 #pragma unroll
       for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = xhalf_max(mx);
       const float m_new = fmaxf(m_run, mx * sl2);
       if (m_new > m_run + kLazy) {
         const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -442,17 +485,10 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       }
     }
 
-    // Next tile: registers -> the other LDS buffer, then refill the registers.
-    if (it + 1 < nt) {
-      const int nx = (u + 1) % PF;         // a constant once the u loop is unrolled
-      kv.store(smem[1 - u][0], smem[1 - u][1], rk[nx], rv[nx]);
-      if (it + 1 + PF < nt)
-        kv.load(rk[nx], rv[nx], a, w, tile_k0(it + 1 + PF), it + 1 + PF == ntp, s_pg);
-    }
-    __syncthreads();
   }
   }
   if constexpr (KW == 2) {
+    __syncthreads();                           // the ring is free (no load is pending)
     // Merge the two key halves of each row through LDS (the tiles are free).
     constexpr int SLOT = NB * 16 + 2;
     float* xs = reinterpret_cast<float*>(&smem[0][0][0]) + (rw * 64 + lane) * SLOT;
@@ -477,7 +513,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
     l_run = l_run * a0 + l1 * a1;
     m_run = mm;
   }
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = xhalf_sum(l_run);
   if (!row_in) return;
 
   // Register j of o[c] holds dim 32*c + 8*(j/4) + 4*h + j%4 of this row.
@@ -534,8 +570,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
   if (!setup_work(a, w)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
-  if (tid < kMaxNew)
-    vis[tid] = tid < a.n_new ? visibility_word(tid, step_row, w.gamma, a.B, a.n_new) : 0ull;
+  build_visibility<NT / 64>(vis, step_row[min(lane, a.B - 1)], w.gamma, a.B, a.n_new, wave, lane);
   if (tid < 32) {
     sm[tid] = kNegInf;
     sl[tid] = 0.f;
@@ -651,39 +686,71 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 template <int D, typename OutT>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int D4 = D / 4;
+  constexpr int SB = 8;                        // splits merged per round of loads
+  // A zero the compiler cannot see through: keeps the per-sequence reads
+  // vector loads issued with the others instead of late scalar loads.
+  int lane_zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(lane_zero));
   const int b = blockIdx.z;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
-  const int plen = min(max(a.prefix_lens[b], 0), a.max_prefix);
-  const int nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
-  if (nsplit <= 1) return;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   const int rowl = idx / D4, d0 = (idx % D4) * 4;
-  if (rowl >= a.rows_pb) return;
-  const int m = rb * a.rows_pb + rowl;
-  if (m >= a.rows) return;
+  const int rl = min(rowl, a.rows_pb - 1);
+  const int m = min(rb * a.rows_pb + rl, a.rows - 1);
   const int t = m / a.group, hq = kvh * a.group + m % a.group;
-  const int gamma = min(max(a.num_ref[b], 0), a.L);
-  // A row is padding iff it sees no new slot (a non-padded row always sees itself).
-  bool valid;
-  if (t < a.B) valid = a.step_map[static_cast<int64_t>(b) * a.B + t] >= 0;
-  else valid = (t - a.B) < gamma;
 
+  // First round of loads, none waiting on another.  Indices are clamped so
+  // every load is in bounds; split blocks past this sequence's count (stale
+  // workspace) are loaded but never used.
+  const int plen_raw = a.prefix_lens[b + lane_zero];
+  const int nref = a.num_ref[b + lane_zero];
+  const int step = a.step_map[static_cast<int64_t>(b) * a.B + min(t, a.B - 1)];
   const int64_t pair = (static_cast<int64_t>(b) * a.hkv + kvh) * a.row_blocks + rb;
   const int64_t pstride = static_cast<int64_t>(a.rows_pb) * (D + 2);
   const float* base = a.part + pair * a.splits * pstride;
   const int mo = a.rows_pb * D;
-  float mt = kNegInf;
-  for (int s = 0; s < nsplit; ++s) mt = fmaxf(mt, base[s * pstride + mo + rowl]);
-  float lsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  if (valid && mt != kNegInf) {
-#pragma unroll 4
-    for (int s = 0; s < nsplit; ++s) {
-      const float* ps = base + s * pstride;
-      const float wt = __builtin_amdgcn_exp2f(ps[mo + rowl] - mt);
-      lsum += wt * ps[mo + a.rows_pb + rowl];
-      acc += wt * *reinterpret_cast<const f32x4*>(ps + rowl * D + d0);
+  float mv[SB], lv[SB];
+  f32x4 ov[SB];
+  auto load_round = [&](int s0) {
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      const float* ps = base + min(s0 + s, a.splits - 1) * pstride;
+      mv[s] = ps[mo + rl];
+      lv[s] = ps[mo + a.rows_pb + rl];
+      ov[s] = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
     }
+  };
+  load_round(0);
+
+  const int plen = min(max(plen_raw, 0), a.max_prefix);
+  const int nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
+  if (nsplit <= 1 || rowl >= a.rows_pb || rb * a.rows_pb + rowl >= a.rows) return;
+  const int gamma = min(max(nref, 0), a.L);
+  // A row is padding iff it sees no new slot (a non-padded row always sees itself).
+  const bool valid = t < a.B ? step >= 0 : (t - a.B) < gamma;
+
+  float mt = kNegInf, lsum = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s0 = 0; s0 < nsplit; s0 += SB) {
+    if (s0 > 0) load_round(s0);
+    float mb = kNegInf;
+#pragma unroll
+    for (int s = 0; s < SB; ++s)
+      if (s0 + s < nsplit) mb = fmaxf(mb, mv[s]);
+    const float mn = fmaxf(mt, mb);
+    if (mn == kNegInf) continue;
+    const float alpha = __builtin_amdgcn_exp2f(mt - mn);   // 0 while mt is -inf
+    lsum *= alpha;
+    acc *= alpha;
+#pragma unroll
+    for (int s = 0; s < SB; ++s) {
+      if (s0 + s < nsplit) {
+        const float wt = __builtin_amdgcn_exp2f(mv[s] - mn);
+        lsum += wt * lv[s];
+        acc += wt * ov[s];
+      }
+    }
+    mt = mn;
   }
   const bool ok = valid && lsum > 0.f;
   const float inv = ok ? 1.f / lsum : 0.f;
@@ -700,11 +767,17 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 }
 
 template <int D, bool PAGED>
-void launch_bf16(int row_waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
+void launch_bf16(int row_waves, int nbuf, dim3 grid, const AttnArgs& a, hipStream_t st) {
   switch (row_waves) {
-    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
+    case 2:
+      if (nbuf == 4) hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, 4, PAGED>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, 2, PAGED>), grid, dim3(256), 0, st, a);
+      break;
+    case 4:
+      if (nbuf == 4) hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, 4, PAGED>), grid, dim3(256), 0, st, a);
+      else hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, 2, PAGED>), grid, dim3(256), 0, st, a);
+      break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, 4, PAGED>), grid, dim3(512), 0, st, a); break;
   }
 }
 
@@ -722,11 +795,11 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const bool paged = d.page_size > 0;
   if (d.dtype == SIMSD_BF16) {
     if (d.head_dim == 128) {
-      if (paged) launch_bf16<128, true>(p.row_waves, grid, a, st);
-      else launch_bf16<128, false>(p.row_waves, grid, a, st);
+      if (paged) launch_bf16<128, true>(p.row_waves, p.nbuf, grid, a, st);
+      else launch_bf16<128, false>(p.row_waves, p.nbuf, grid, a, st);
     } else {
-      if (paged) launch_bf16<64, true>(p.row_waves, grid, a, st);
-      else launch_bf16<64, false>(p.row_waves, grid, a, st);
+      if (paged) launch_bf16<64, true>(p.row_waves, p.nbuf, grid, a, st);
+      else launch_bf16<64, false>(p.row_waves, p.nbuf, grid, a, st);
     }
   } else {
     if (d.head_dim == 128) launch_f32<128>(paged, grid, a, st);
