@@ -25,6 +25,8 @@
 // as the B operand; the V^T operand comes from LDS transpose reads
 // (ds_read_b64_tr_b16), so no register shuffles are needed.  Row maxima are
 // kept in log2 units and rescaled only when they grow by more than 2^8.
+#include <type_traits>
+
 #include "simsd_kernels.h"
 
 namespace simsd {
@@ -178,10 +180,21 @@ constexpr int kMaxChunkPages = 512;            // page ids of one chunk staged i
 // It counts in vmcnt like any vector load but the compiler does not track it:
 // readers wait with wait_vm and then pass a barrier.  M0 (the LDS base) is a
 // reserved register that the compiler does not allocate to values, so setting
-// it here disturbs nothing.
+// it here disturbs nothing.  dma16s takes a wave-uniform 64-bit base and a
+// 32-bit per-lane offset (no per-lane address arithmetic).
 __device__ inline void dma16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+__device__ inline void dma16s(const void* base, uint32_t voff, uint32_t lds) {
+  // readfirstlane works on (signed) int: each half goes through uint32_t
+  // before widening so that the low half is not sign-extended.
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b & 0xffffffffu)));
+  const uint64_t bu = (static_cast<uint64_t>(hi) << 32) | lo;
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
+               :: "v"(voff), "s"(bu), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
 template <int N>
 __device__ inline void wait_vm() {
@@ -196,9 +209,10 @@ __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_b
 // slots with direct loads.  One instruction covers RPI key rows of one
 // tensor; lane i writes chunk position i % CPR of row i / CPR of its block
 // and so fetches logical chunk (i % CPR) ^ swz(row).  The tiles are split
-// between the waves by instruction.  Rows past the prefix (the tail tile) or
-// past the new slots (the new-slot tile) read the last valid row instead:
-// their scores are masked and their values are finite, so they add zeros.
+// between the waves by instruction.  Full tiles (and the new-slot tile) use a
+// wave-uniform base plus a fixed lane offset; rows past the prefix (the tail
+// tile) or past the new slots read the last valid row instead: their scores
+// are masked and their values are finite, so they add exact zeros.
 template <int D, int NW, bool PAGED>
 struct KVRing {
   static constexpr int ROWB = TileGeom<D>::ROWB, TILEB = TileGeom<D>::TILEB;
@@ -208,33 +222,33 @@ struct KVRing {
   static constexpr int PERW = 2 * IPT / NW;    // instructions per wave per tile
   static_assert(PERW >= 1 && (2 * IPT) % NW == 0, "tile instructions split evenly over the waves");
 
-  const char* kc;
+  const char* kc;         // caches, offset to this KV head
   const char* vc;
-  const char* kn;
+  const char* kn;         // new slots, offset to (sequence, KV head, slot 0)
   const char* vn;
   int64_t seqoff;         // contiguous: this sequence's cache offset (bytes)
   int64_t tokb, pageb;    // bytes per token, per page
-  int64_t hoff;           // this KV head (bytes)
-  int64_t newoff, newrow; // new slots: offset of slot 0 of (sequence, KV head), bytes per slot
-  int64_t loff[PERW];     // full tiles: per-instruction lane offset (bytes)
-  int pgrel[PERW];        // paged full tiles: page of the row relative to the tile's first
+  int64_t newrow;         // bytes per new slot
+  uint32_t voff[PERW];    // fast path: lane offset of instruction i (bytes)
   int row[PERW], chunk[PERW];
   int wave, P, pg_first, n_new;
   bool lds_pages;         // page ids of this chunk are staged in s_pg
+  bool fast;              // full tiles take the uniform-base path
   const int32_t* bt;      // this sequence's block table row
 
-  __device__ inline void init(const AttnArgs& a, const Work& w, int tid, int* s_pg) {
-    wave = tid >> 6;
-    const int lane = tid & 63;
-    kc = static_cast<const char*>(a.k_cache);
-    vc = static_cast<const char*>(a.v_cache);
-    kn = static_cast<const char*>(a.k_new);
-    vn = static_cast<const char*>(a.v_new);
-    tokb = a.cs_tok * 2;
-    hoff = static_cast<int64_t>(w.kvh) * a.cs_head * 2;
-    n_new = a.n_new;
+  __device__ __attribute__((always_inline)) void init(const AttnArgs& a, const Work& w, int wave_, int lane, int* s_pg) {
+    wave = wave_;
+    const int64_t hoff = static_cast<int64_t>(w.kvh) * a.cs_head * 2;
+    kc = static_cast<const char*>(a.k_cache) + hoff;
+    vc = static_cast<const char*>(a.v_cache) + hoff;
     newrow = static_cast<int64_t>(a.hkv) * D * 2;
-    newoff = (static_cast<int64_t>(w.b) * a.n_new * a.hkv + w.kvh) * D * 2;
+    const int64_t newoff = (static_cast<int64_t>(w.b) * a.n_new * a.hkv + w.kvh) * D * 2;
+    kn = static_cast<const char*>(a.k_new) + newoff;
+    vn = static_cast<const char*>(a.v_new) + newoff;
+    tokb = a.cs_tok * 2;
+    n_new = a.n_new;
+    // Lane offsets of a tile must fit 32 bits: 64 rows of tokb bytes.
+    fast = tokb < (int64_t{1} << 25);
     if (PAGED) {
       P = a.page_size;
       pageb = a.cs_seq * 2;
@@ -243,7 +257,9 @@ struct KVRing {
       const int npg = w.kend > w.kbeg ? (w.kend - 1) / P - pg_first + 1 : 0;
       lds_pages = (kTile % P == 0) && npg <= kMaxChunkPages;
       if (lds_pages)
-        for (int j = tid; j < npg; j += NW * 64) s_pg[j] = bt[pg_first + j];
+        for (int j = wave * 64 + lane; j < npg; j += NW * 64) s_pg[j] = bt[pg_first + j];
+      // One page per instruction: the instruction's RPI rows share a page.
+      fast = fast && lds_pages && P % RPI == 0;
     } else {
       seqoff = static_cast<int64_t>(w.b) * a.cs_seq * 2;
     }
@@ -252,44 +268,42 @@ struct KVRing {
       const int g = wave * PERW + i;
       row[i] = (g % IPT) * RPI + lane / CPR;
       chunk[i] = (lane % CPR) ^ swz<D>(row[i]);
-      if (PAGED) {
-        pgrel[i] = lds_pages ? row[i] / P : 0;
-        loff[i] = static_cast<int64_t>(lds_pages ? row[i] % P : 0) * tokb + hoff + chunk[i] * 16;
-      } else {
-        loff[i] = static_cast<int64_t>(row[i]) * tokb + hoff + chunk[i] * 16;
-      }
+      const int r = PAGED ? (P > 0 ? row[i] % P : 0) : row[i];
+      voff[i] = static_cast<uint32_t>(static_cast<int64_t>(r) * tokb + chunk[i] * 16);
     }
   }
 
-  // Byte offset of (key, this head, element 0) in the cache (general path).
-  __device__ inline int64_t key_offset(int key, const int* s_pg) const {
-    if (!PAGED) return seqoff + static_cast<int64_t>(key) * tokb + hoff;
+  // Byte offset of (key, element 0) from this head's cache base (general path).
+  __device__ __attribute__((always_inline)) int64_t key_offset(int key, const int* s_pg) const {
+    if (!PAGED) return seqoff + static_cast<int64_t>(key) * tokb;
     const int64_t page = lds_pages ? s_pg[key / P - pg_first] : bt[key / P];
-    return page * pageb + static_cast<int64_t>(key % P) * tokb + hoff;
+    return page * pageb + static_cast<int64_t>(key % P) * tokb;
   }
 
   // Issue this wave's share of the tile starting at prefix key k0 (or of the
   // new-slot tile) into the ring slot at LDS byte address `slot`.
-  __device__ inline void issue(uint32_t slot, int k0, bool is_new, int kend, const int* s_pg) const {
+  __device__ __attribute__((always_inline)) void issue(uint32_t slot, int k0, bool is_new, int kend, const int* s_pg) const {
     if (is_new) {
 #pragma unroll
       for (int i = 0; i < PERW; ++i) {
         const int g = wave * PERW + i;
-        const int r = min(row[i], n_new - 1);
-        const char* src = (g < IPT ? kn : vn) + newoff + r * newrow + chunk[i] * 16;
-        dma16(src, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
+        const uint32_t off = static_cast<uint32_t>(min(row[i], n_new - 1) * newrow) + chunk[i] * 16;
+        dma16s(g < IPT ? kn : vn, off, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
-    } else if (k0 + kTile <= kend && (!PAGED || lds_pages)) {
-      int64_t tbase = 0;
-      int pbase = 0;
-      if (PAGED) pbase = k0 / P - pg_first;
-      else tbase = seqoff + static_cast<int64_t>(k0) * tokb;
+    } else if (k0 + kTile <= kend && fast) {
 #pragma unroll
       for (int i = 0; i < PERW; ++i) {
         const int g = wave * PERW + i;
-        const int64_t off = PAGED ? static_cast<int64_t>(s_pg[pbase + pgrel[i]]) * pageb + loff[i]
-                                  : tbase + loff[i];
-        dma16((g < IPT ? kc : vc) + off, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
+        // Paged: the instruction's rows lie in one page (P is a multiple of
+        // RPI and k0 of P); the lane offset holds the row within the page.
+        int64_t base;
+        if (PAGED) {
+          const int pg = __builtin_amdgcn_readfirstlane(s_pg[(k0 + (g % IPT) * RPI) / P - pg_first]);
+          base = static_cast<int64_t>(pg) * pageb;
+        } else {
+          base = seqoff + static_cast<int64_t>(k0) * tokb;
+        }
+        dma16s((g < IPT ? kc : vc) + base, voff[i], slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
     } else {
 #pragma unroll
@@ -306,10 +320,14 @@ struct KVRing {
 // RW row waves of 32 rows each; KW = 2 pairs every row wave with a second wave
 // that takes the other 32-key half of each tile (small row blocks, where the
 // extra wave doubles the work in flight); the two halves merge at the end.
-// NBUF tiles of the ring: tile it + NBUF - 1 loads while tile it is read.
-template <int D, int RW, int KW, int NBUF, bool PAGED>
+// The ring holds NBUF tiles: tile it + NBUF - 1 loads while tile it is read.
+// The 8-wave group has a CU to itself (its registers allow no second group)
+// and keeps three tiles in flight; 4-wave groups run two to a CU, each with a
+// two-tile ring (measured faster than one group with a deeper ring).
+template <int D, int RW, int KW, bool PAGED>
 __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   constexpr int NW = RW * KW;
+  constexpr int NBUF = NW >= 8 ? 4 : 2;
   constexpr int NB = D / 32;                   // 32-dim output blocks
   constexpr int KS = D / 16;                   // k-steps of QK^T
   constexpr int ROWB = TileGeom<D>::ROWB;
@@ -321,7 +339,8 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
 
   Work w;
   if (!setup_work(a, w)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int n = lane & 31, h = lane >> 5;
   const int rw = wave % RW, kw = wave / RW;    // row wave, key half
 
@@ -352,7 +371,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
     }
   }
   Ring kv;
-  kv.init(a, w, tid, s_pg);
+  kv.init(a, w, wave, lane, s_pg);
   if (PAGED) __syncthreads();                  // staged page ids
 
   const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
@@ -396,12 +415,11 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       }
   }
 
-  // The loop is unrolled by NBUF so that ring slots are compile-time offsets.
-  for (int it0 = 0; it0 < nt; it0 += NBUF) {
-#pragma unroll
-  for (int u = 0; u < NBUF; ++u) {
-    const int it = it0 + u;
-    if (it >= nt) break;
+  // One tile: wait for it, free the slot of the previous tile for the next
+  // load, then its key blocks.  `masked` tiles (the prefix tail and the
+  // new-slot tile) take the mask code; full prefix tiles take a copy without
+  // it.  `sl` is the tile's ring slot.
+  auto tile = [&](auto masked, int it, int sl) __attribute__((always_inline)) {
     const bool is_new = it == ntp;
     const int k0 = tile_k0(it);
     // This wave's share of tile `it` has landed once at most the loads of the
@@ -413,10 +431,10 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
     lds_barrier();                             // all of tile `it` is in; slot of tile it-1 is free
     if (it + NBUF - 1 < nt) {
       const int nx = it + NBUF - 1;
-      kv.issue(ring0 + ((u + NBUF - 1) % NBUF) * kSlotBytes, tile_k0(nx), nx == ntp, w.kend, s_pg);
+      kv.issue(ring0 + ((sl + NBUF - 1) % NBUF) * kSlotBytes, tile_k0(nx), nx == ntp, w.kend, s_pg);
     }
-    const uint8_t* sk = smem[u][0];
-    const uint8_t* sv = smem[u][1];
+    const uint8_t* sk = &smem[0][0][0] + sl * kSlotBytes;
+    const uint8_t* sv = sk + TILEB;
 
 #pragma unroll
     for (int kb0 = 0; kb0 < 2 / KW; ++kb0) {
@@ -431,17 +449,19 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
         const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sk + 32 * kb * ROWB + koff[ks]);
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s, 0, 0, 0);
       }
-      if (is_new) {
+      if constexpr (decltype(masked)::value) {
+        if (is_new) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int key = 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-          if (!((myvis >> key) & 1ull)) s[j] = kNegInf;
-        }
-      } else if (k0 + kTile > w.kend) {
+          for (int j = 0; j < 16; ++j) {
+            const int key = 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
+            if (!((myvis >> key) & 1ull)) s[j] = kNegInf;
+          }
+        } else {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int key = k0 + 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-          if (key >= w.kend) s[j] = kNegInf;
+          for (int j = 0; j < 16; ++j) {
+            const int key = k0 + 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
+            if (key >= w.kend) s[j] = kNegInf;
+          }
         }
       }
 
@@ -484,9 +504,19 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
         }
       }
     }
+  };
 
+  // Full prefix tiles, unrolled by NBUF so that ring slots are compile-time
+  // offsets; then the masked tiles (at most the prefix tail and the new slots).
+  const int nfull = (w.kend - w.kbeg) / kTile;
+  for (int it0 = 0; it0 < nfull; it0 += NBUF) {
+#pragma unroll
+    for (int u = 0; u < NBUF; ++u) {
+      if (it0 + u >= nfull) break;
+      tile(std::false_type{}, it0 + u, u);
+    }
   }
-  }
+  for (int it = nfull; it < nt; ++it) tile(std::true_type{}, it, it % NBUF);
   if constexpr (KW == 2) {
     __syncthreads();                           // the ring is free (no load is pending)
     // Merge the two key halves of each row through LDS (the tiles are free).
@@ -767,17 +797,11 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 }
 
 template <int D, bool PAGED>
-void launch_bf16(int row_waves, int nbuf, dim3 grid, const AttnArgs& a, hipStream_t st) {
+void launch_bf16(int row_waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
   switch (row_waves) {
-    case 2:
-      if (nbuf == 4) hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, 4, PAGED>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, 2, PAGED>), grid, dim3(256), 0, st, a);
-      break;
-    case 4:
-      if (nbuf == 4) hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, 4, PAGED>), grid, dim3(256), 0, st, a);
-      else hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, 2, PAGED>), grid, dim3(256), 0, st, a);
-      break;
-    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, 4, PAGED>), grid, dim3(512), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
   }
 }
 
@@ -795,11 +819,11 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const bool paged = d.page_size > 0;
   if (d.dtype == SIMSD_BF16) {
     if (d.head_dim == 128) {
-      if (paged) launch_bf16<128, true>(p.row_waves, p.nbuf, grid, a, st);
-      else launch_bf16<128, false>(p.row_waves, p.nbuf, grid, a, st);
+      if (paged) launch_bf16<128, true>(p.row_waves, grid, a, st);
+      else launch_bf16<128, false>(p.row_waves, grid, a, st);
     } else {
-      if (paged) launch_bf16<64, true>(p.row_waves, p.nbuf, grid, a, st);
-      else launch_bf16<64, false>(p.row_waves, p.nbuf, grid, a, st);
+      if (paged) launch_bf16<64, true>(p.row_waves, grid, a, st);
+      else launch_bf16<64, false>(p.row_waves, grid, a, st);
     }
   } else {
     if (d.head_dim == 128) launch_f32<128>(paged, grid, a, st);

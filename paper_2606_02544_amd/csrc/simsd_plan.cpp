@@ -96,11 +96,6 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   }
   r.splits = d->max_prefix_len > 0 ? static_cast<int>(ceil_div(d->max_prefix_len, r.chunk)) : 1;
   if (r.splits > 65535 * 1024) return fail(SIMSD_ERR_BAD_SHAPE, "attention: too many splits");
-  // LDS ring depth: four tiles (three loading while one is read) for the
-  // 8-wave group, which has the CU to itself anyway, and for chunks short
-  // enough that the whole chunk plus the new-slot tile is then in flight at
-  // once; otherwise two, so that two 4-wave groups share a CU.
-  r.nbuf = (r.waves >= 8 || r.chunk / kTile + 1 <= 4) ? 4 : 2;
   r.part_floats = static_cast<size_t>(r.rows_pb) * (d->head_dim + 2);
   r.workspace = r.splits > 1 ? static_cast<size_t>(r.pairs) * r.splits * r.part_floats * 4 : 0;
   const float scale = d->scale > 0.f ? d->scale : 1.0f / std::sqrt(static_cast<float>(d->head_dim));

@@ -29,7 +29,6 @@ struct AttnPlan {
   int row_blocks = 0;   // ceil(rows / rows_pb)
   int chunk = 0;        // prefix keys per split
   int splits = 0;       // grid.x: ceil(max_prefix_len / chunk), >= 1
-  int nbuf = 0;         // bf16: K/V tiles in the LDS ring (2 or 4)
   int64_t pairs = 0;    // batch * Hkv * row_blocks
   size_t part_floats = 0;   // floats per split partial: rows_pb * (head_dim + 2)
   size_t workspace = 0;     // total bytes
