@@ -231,8 +231,8 @@ struct KVRing {
   int64_t newrow;         // bytes per new slot
   uint32_t voff[PERW];    // fast path: lane offset of instruction i (bytes)
   int row[PERW], chunk[PERW];
-  int wave, P, pg_first, n_new;
-  bool lds_pages;         // page ids of this chunk are staged in s_pg
+  int wave, P, lgP, pg_first, n_new;
+  bool lds_pages;         // page ids of this chunk are staged in s_pg (P divides 64)
   bool fast;              // full tiles take the uniform-base path
   const int32_t* bt;      // this sequence's block table row
 
@@ -256,6 +256,7 @@ struct KVRing {
       pg_first = w.kbeg / P;
       const int npg = w.kend > w.kbeg ? (w.kend - 1) / P - pg_first + 1 : 0;
       lds_pages = (kTile % P == 0) && npg <= kMaxChunkPages;
+      lgP = __builtin_ctz(P);                  // P is a power of two when it divides 64
       if (lds_pages)
         for (int j = wave * 64 + lane; j < npg; j += NW * 64) s_pg[j] = bt[pg_first + j];
       // One page per instruction: the instruction's RPI rows share a page.
@@ -291,18 +292,20 @@ struct KVRing {
         dma16s(g < IPT ? kn : vn, off, slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
     } else if (k0 + kTile <= kend && fast) {
+      // Paged: lane j holds page j of the tile (one LDS read); instruction i's
+      // rows lie in one page (P is a multiple of RPI and k0 of P) and its lane
+      // offsets hold the row within that page.
+      int pgl = 0;
+      if (PAGED) {
+        const int j = min(static_cast<int>(threadIdx.x & 63), (kTile >> lgP) - 1);
+        pgl = s_pg[((k0 - pg_first * P) >> lgP) + j];   // pg_first * P == kbeg
+      }
 #pragma unroll
       for (int i = 0; i < PERW; ++i) {
         const int g = wave * PERW + i;
-        // Paged: the instruction's rows lie in one page (P is a multiple of
-        // RPI and k0 of P); the lane offset holds the row within the page.
         int64_t base;
-        if (PAGED) {
-          const int pg = __builtin_amdgcn_readfirstlane(s_pg[(k0 + (g % IPT) * RPI) / P - pg_first]);
-          base = static_cast<int64_t>(pg) * pageb;
-        } else {
-          base = seqoff + static_cast<int64_t>(k0) * tokb;
-        }
+        if (PAGED) base = static_cast<int64_t>(__builtin_amdgcn_readlane(pgl, ((g % IPT) * RPI) >> lgP)) * pageb;
+        else base = seqoff + static_cast<int64_t>(k0) * tokb;
         dma16s((g < IPT ? kc : vc) + base, voff[i], slot + (g / IPT) * TILEB + (g % IPT) * 1024);
       }
     } else {
