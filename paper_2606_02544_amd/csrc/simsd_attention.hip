@@ -25,6 +25,7 @@
 // as the B operand; the V^T operand comes from LDS transpose reads
 // (ds_read_b64_tr_b16), so no register shuffles are needed.  Row maxima are
 // kept in log2 units and rescaled only when they grow by more than 2^8.
+#include <algorithm>
 #include <type_traits>
 
 #include "simsd_kernels.h"
@@ -728,8 +729,10 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
   const int idx = blockIdx.x * 256 + threadIdx.x;
   const int rowl = idx / D4, d0 = (idx % D4) * 4;
-  const int rl = min(rowl, a.rows_pb - 1);
-  const int m = min(rb * a.rows_pb + rl, a.rows - 1);
+  // Rows past the packed rows of this block have no partials.
+  if (rowl >= a.rows_pb || rb * a.rows_pb + rowl >= a.rows) return;
+  const int rl = rowl;
+  const int m = rb * a.rows_pb + rl;
   const int t = m / a.group, hq = kvh * a.group + m % a.group;
 
   // First round of loads, none waiting on another.  Indices are clamped so
@@ -757,7 +760,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 
   const int plen = min(max(plen_raw, 0), a.max_prefix);
   const int nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
-  if (nsplit <= 1 || rowl >= a.rows_pb || rb * a.rows_pb + rowl >= a.rows) return;
+  if (nsplit <= 1) return;
   const int gamma = min(max(nref, 0), a.L);
   // A row is padding iff it sees no new slot (a non-padded row always sees itself).
   const bool valid = t < a.B ? step >= 0 : (t - a.B) < gamma;
@@ -834,7 +837,8 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits <= 1) return e;
-  const int per_block = (p.rows_pb * d.head_dim / 4 + 255) / 256;
+  // Threads for the packed rows only (the last row block may be partial).
+  const int per_block = (std::min(p.rows_pb, p.rows) * d.head_dim / 4 + 255) / 256;
   const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
   const bool bf16 = d.dtype == SIMSD_BF16;
   if (d.head_dim == 128) {
