@@ -322,12 +322,13 @@ struct KVRing {
 };
 
 // RW row waves of 32 rows each; KW = 2 pairs every row wave with a second wave
-// that takes the other 32-key half of each tile (small row blocks, where the
-// extra wave doubles the work in flight); the two halves merge at the end.
+// that takes the other 32-key half of each tile (row blocks of up to 128 rows,
+// where the extra waves double the work in flight); the two halves merge at
+// the end.
 // The ring holds NBUF tiles: tile it + NBUF - 1 loads while tile it is read.
-// The 8-wave group has a CU to itself (its registers allow no second group)
-// and keeps three tiles in flight; 4-wave groups run two to a CU, each with a
-// two-tile ring (measured faster than one group with a deeper ring).
+// 8-wave groups have a CU to themselves (their registers allow no second
+// group) and keep three tiles in flight; 4-wave groups run two to a CU, each
+// with a two-tile ring (measured faster than one group with a deeper ring).
 template <int D, int RW, int KW, bool PAGED>
 __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   constexpr int NW = RW * KW;
@@ -806,7 +807,7 @@ template <int D, bool PAGED>
 void launch_bf16(int row_waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
   switch (row_waves) {
     case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
   }
 }

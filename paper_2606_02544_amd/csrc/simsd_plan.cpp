@@ -66,12 +66,12 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   r.rows = r.group * r.n_new;
   if (d->dtype == SIMSD_BF16) {
     // One 32-row MFMA block per row wave; a power of two in [2, 8].  With two
-    // row waves, each is paired with a second wave taking the other half of
-    // every key tile.
+    // or four row waves, each is paired with a second wave taking the other
+    // half of every key tile (4 or 8 waves per group).
     const int need = static_cast<int>(ceil_div(std::min(r.rows, 256), 32));
     r.row_waves = 2;
     while (r.row_waves < need) r.row_waves *= 2;
-    r.waves = r.row_waves == 2 ? 4 : r.row_waves;
+    r.waves = r.row_waves <= 4 ? 2 * r.row_waves : r.row_waves;
     r.rows_pb = r.row_waves * 32;
   } else {
     r.waves = 4;          // 8 rows per wave, one wave per row at a time

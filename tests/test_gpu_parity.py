@@ -70,6 +70,8 @@ MIXED = [
     ("bf16", 128, 32, 8, 8, 0, (64, 64), 0, 0, 6),
     ("bf16", 128, 12, 4, 3, 2, (0, 0), 0, 0, 7),
     ("bf16", 128, 16, 2, 32, 32, (100, 400), 16, 64, 8),
+    ("bf16", 64, 8, 2, 16, 16, (100, 300), 16, 64, 13),     # 128 rows: 4 row waves x 2
+    ("bf16", 128, 12, 3, 24, 8, (0, 700), 32, 128, 14),     # 128 rows, paged, tail tiles
     ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
     ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
     ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
