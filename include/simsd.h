@@ -113,8 +113,11 @@ typedef struct {
   int32_t page_size;          /* 0 = contiguous cache; else tokens per page       */
   int32_t max_pages_per_seq;  /* paged: block_table row length,
                                  >= ceil(max_prefix_len / page_size)              */
-  int32_t kv_chunk;           /* prefix keys per work-group (multiple of 64), or
-                                 0 to let the library choose                      */
+  int32_t kv_chunk;           /* prefix keys per work-group (multiple of 64);
+                                 0 to let the library choose; -1 for the stream
+                                 decomposition (equal tile ranges per resident
+                                 work-group; bf16, Hq/Hkv*(B+L) <= 128 and
+                                 batch <= 256 only, else SIMSD_ERR_UNSUPPORTED) */
   int64_t cache_stride_seq;   /* elements between sequences (contiguous) / pages  */
   int64_t cache_stride_token; /* elements between consecutive tokens              */
   int64_t cache_stride_head;  /* elements between consecutive KV heads            */

@@ -40,6 +40,12 @@ extern "C" simsd_status simsd_verify_attention(
     a.out = out;
     a.lse = lse;
     a.part = p.workspace ? static_cast<float*>(workspace) : nullptr;
+    a.stream_groups = p.stream ? p.stream_groups : 0;
+    a.stream_seq0 = p.stream ? reinterpret_cast<int64_t*>(static_cast<char*>(workspace) +
+                                                          static_cast<size_t>(p.stream_groups) * 2 *
+                                                              p.part_floats * 4)
+                             : nullptr;
+    a.batch = desc->batch;
     a.cs_seq = desc->cache_stride_seq;
     a.cs_tok = desc->cache_stride_token;
     a.cs_head = desc->cache_stride_head;

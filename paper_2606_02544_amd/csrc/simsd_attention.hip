@@ -92,12 +92,20 @@ __device__ inline void build_visibility(uint64_t* vis, int step, int gamma, int 
   }
 }
 
-// Which prefix keys a work-group owns.
+// One contiguous key range of one (sequence, KV head, row block) pair that a
+// work-group attends over: prefix keys [kbeg, kend), plus the new-slot tile
+// when has_new.  A range that covers the whole pair (final) writes the
+// normalised output; any other writes an unnormalised partial to `part`.
 struct Work {
   int split, kvh, rb, b, plen, nsplit, kbeg, kend, gamma;
+  bool has_new, final;
+  float* part;
 };
 
-__device__ inline bool setup_work(const AttnArgs& a, Work& w) {
+__device__ inline float* partial_base(const AttnArgs& a, const Work& w, int D);
+
+// Chunked decomposition: work-group (split, KV head x row block, sequence).
+__device__ inline bool setup_work(const AttnArgs& a, Work& w, int D) {
   w.split = blockIdx.x;
   w.kvh = blockIdx.y / a.row_blocks;
   w.rb = blockIdx.y % a.row_blocks;
@@ -108,6 +116,9 @@ __device__ inline bool setup_work(const AttnArgs& a, Work& w) {
   w.kbeg = w.split * a.chunk;
   w.kend = min(w.plen, w.kbeg + a.chunk);
   w.gamma = min(max(a.num_ref[w.b], 0), a.L);
+  w.has_new = w.split == 0;
+  w.final = w.nsplit == 1;
+  w.part = w.final ? nullptr : partial_base(a, w, D);
   return true;
 }
 
@@ -174,7 +185,7 @@ __device__ inline int swz(int r) {
     return ((r & 1) ? 2 : 0) ^ ((r & 2) ? 4 : 0) ^ ((r & 4) ? 1 : 0) ^ ((r & 8) ? 2 : 0);
 }
 
-constexpr int kMaxChunkPages = 512;            // page ids of one chunk staged in LDS
+constexpr int kMaxChunkPages = 2048;           // page ids of one key range staged in LDS
 
 // Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
 // lane i's bytes land at LDS byte lds + 16 * i, so one instruction moves 1 KB.
@@ -330,7 +341,7 @@ struct KVRing {
 // group) and keep three tiles in flight; 4-wave groups run two to a CU, each
 // with a two-tile ring (measured faster than one group with a deeper ring).
 template <int D, int RW, int KW, bool PAGED>
-__global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
+__device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a, const Work& w) {
   constexpr int NW = RW * KW;
   constexpr int NBUF = NW >= 8 ? 4 : 2;
   constexpr int NB = D / 32;                   // 32-dim output blocks
@@ -342,8 +353,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
   __shared__ uint64_t vis[kMaxNew];
   __shared__ int s_pg[PAGED ? kMaxChunkPages : 1];
 
-  Work w;
-  if (!setup_work(a, w)) return;
+  __syncthreads();                             // the work-group's previous range is done with the LDS
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int n = lane & 31, h = lane >> 5;
@@ -380,13 +390,14 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
   if (PAGED) __syncthreads();                  // staged page ids
 
   const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
-  const int nt = ntp + (w.split == 0 ? 1 : 0);
+  const int nt = ntp + (w.has_new ? 1 : 0);
   auto tile_k0 = [&](int it) { return w.kbeg + it * kTile; };
   const uint32_t ring0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
       (SIMSD_LDS void*)(&smem[0][0][0])));      // LDS byte address of slot 0
   constexpr uint32_t kSlotBytes = 2 * TILEB;
+  // Every slot is free at the start: the first NBUF tiles load at once.
 #pragma unroll
-  for (int j = 0; j < NBUF - 1; ++j)
+  for (int j = 0; j < NBUF; ++j)
     if (j < nt) kv.issue(ring0 + j * kSlotBytes, tile_k0(j), j == ntp, w.kend, s_pg);
 
   build_visibility<NW>(vis, lane_step, w.gamma, a.B, a.n_new, wave, lane);
@@ -428,77 +439,99 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
     const bool is_new = it == ntp;
     const int k0 = tile_k0(it);
     // This wave's share of tile `it` has landed once at most the loads of the
-    // younger tiles remain (vector memory completes in issue order).
-    const int younger = min(nt - 1, it + NBUF - 2) - it;
-    if (NBUF >= 4 && younger >= 2) wait_vm<2 * Ring::PERW>();
-    else if (NBUF >= 3 && younger >= 1) wait_vm<Ring::PERW>();
+    // younger tiles remain (vector memory completes in issue order).  Tiles
+    // issued so far: the first NBUF, then one per earlier iteration.
+    const int younger = min(nt - 1, max(NBUF - 1, it + NBUF - 2)) - it;
+    if (NBUF >= 4 && younger >= 3) wait_vm<3 * Ring::PERW>();
+    else if (NBUF >= 3 && younger >= 2) wait_vm<2 * Ring::PERW>();
+    else if (younger >= 1) wait_vm<Ring::PERW>();
     else wait_vm<0>();
     lds_barrier();                             // all of tile `it` is in; slot of tile it-1 is free
-    if (it + NBUF - 1 < nt) {
+    if (it >= 1 && it + NBUF - 1 < nt) {
       const int nx = it + NBUF - 1;
       kv.issue(ring0 + ((sl + NBUF - 1) % NBUF) * kSlotBytes, tile_k0(nx), nx == ntp, w.kend, s_pg);
     }
-    const uint8_t* sk = &smem[0][0][0] + sl * kSlotBytes;
-    const uint8_t* sv = sk + TILEB;
+    // LDS-typed pointers (no generic-pointer arithmetic on the ring).
+    const SIMSD_LDS uint8_t* sk = reinterpret_cast<const SIMSD_LDS uint8_t*>(ring0) + sl * kSlotBytes;
+    const SIMSD_LDS uint8_t* sv = sk + TILEB;
 
+    // The wave's key blocks of this tile, one at a time: both 32-key blocks
+    // when KW == 1, block kw when KW == 2.  (Taking both blocks' scores at
+    // once measured no faster and needs 16 more registers.)
 #pragma unroll
-    for (int kb0 = 0; kb0 < 2 / KW; ++kb0) {
-      const int kb = KW == 1 ? kb0 : kw;
-      // S^T = K Q^T for one 32-key block.  Register j holds key
-      // 32*kb + 8*(j/4) + 4*h + j%4 of this lane's row.
-      f32x16 s;
+    for (int kb1 = 0; kb1 < 2 / KW; ++kb1) {
+    constexpr int NKB = 1;
+    f32x16 s[NKB];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) s[j] = 0.f;
+    for (int q = 0; q < NKB; ++q)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(sk + 32 * kb * ROWB + koff[ks]);
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s, 0, 0, 0);
+      for (int j = 0; j < 16; ++j) s[q][j] = 0.f;
+    // S^T = K Q^T.  Register j of s[q] holds key 32*kb + 8*(j/4) + 4*h + j%4
+    // of this lane's row, kb = the block of s[q].
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int q = 0; q < NKB; ++q) {
+        const int kb = KW == 1 ? kb1 : kw;
+        const bf16x8 ka = *reinterpret_cast<const SIMSD_LDS bf16x8*>(sk + 32 * kb * ROWB + koff[ks]);
+        s[q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], s[q], 0, 0, 0);
       }
-      if constexpr (decltype(masked)::value) {
+    if constexpr (decltype(masked)::value) {
+#pragma unroll
+      for (int q = 0; q < NKB; ++q) {
+        const int kb = KW == 1 ? kb1 : kw;
         if (is_new) {
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
             const int key = 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-            if (!((myvis >> key) & 1ull)) s[j] = kNegInf;
+            if (!((myvis >> key) & 1ull)) s[q][j] = kNegInf;
           }
         } else {
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
             const int key = k0 + 32 * kb + 8 * (j >> 2) + 4 * h + (j & 3);
-            if (key >= w.kend) s[j] = kNegInf;
+            if (key >= w.kend) s[q][j] = kNegInf;
           }
         }
       }
+    }
 
-      float mx = kNegInf;
+    float mx = kNegInf;
 #pragma unroll
-      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[j]);
-      mx = xhalf_max(mx);
-      const float m_new = fmaxf(m_run, mx * sl2);
-      if (m_new > m_run + kLazy) {
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= alpha;
+    for (int q = 0; q < NKB; ++q)
 #pragma unroll
-        for (int c = 0; c < NB; ++c) o[c] *= alpha;
-        m_run = m_new;
-      }
-      const float moff = m_run == kNegInf ? 0.f : m_run;
+      for (int j = 0; j < 16; ++j) mx = fmaxf(mx, s[q][j]);
+    mx = xhalf_max(mx);
+    const float m_new = fmaxf(m_run, mx * sl2);
+    if (m_new > m_run + kLazy) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int c = 0; c < NB; ++c) o[c] *= alpha;
+      m_run = m_new;
+    }
+    const float moff = m_run == kNegInf ? 0.f : m_run;
+#pragma unroll
+    for (int q = 0; q < NKB; ++q)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[j], sl2, -moff));
-        s[j] = p;
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[q][j], sl2, -moff));
+        s[q][j] = p;
         l_run += p;
       }
 
-      // O^T += V^T P^T, two 16-key chunks.  Chunk hf covers keys
-      // 32*kb + 16*hf + kappa(h, i), kappa(h, i) = 8*(i/4) + 4*h + i%4.
+    // O^T += V^T P^T, two 16-key chunks per block.  Chunk hf of block kb
+    // covers keys 32*kb + 16*hf + kappa(h, i), kappa(h, i) = 8*(i/4) + 4*h + i%4.
+#pragma unroll
+    for (int q = 0; q < NKB; ++q) {
+      const int kb = KW == 1 ? kb1 : kw;
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         u32x4 pw;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) pw[p] = pack2(s[8 * hf + 2 * p], s[8 * hf + 2 * p + 1]);
+        for (int p = 0; p < 4; ++p) pw[p] = pack2(s[q][8 * hf + 2 * p], s[q][8 * hf + 2 * p + 1]);
         const bf16x8 pb = __builtin_bit_cast(bf16x8, pw);
-        const uint8_t* vblk = sv + (32 * kb + 16 * hf) * ROWB;
+        const SIMSD_LDS uint8_t* vblk = sv + (32 * kb + 16 * hf) * ROWB;
 #pragma unroll
         for (int c = 0; c < NB; ++c) {
           const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((SIMSD_LDS s16x4*)(vblk + voff[c][0]));
@@ -508,6 +541,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
           o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vw), pb, o[c], 0, 0, 0);
         }
       }
+    }
     }
   };
 
@@ -526,7 +560,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
     __syncthreads();                           // the ring is free (no load is pending)
     // Merge the two key halves of each row through LDS (the tiles are free).
     constexpr int SLOT = NB * 16 + 2;
-    float* xs = reinterpret_cast<float*>(&smem[0][0][0]) + (rw * 64 + lane) * SLOT;
+    SIMSD_LDS float* xs = reinterpret_cast<SIMSD_LDS float*>(ring0) + (rw * 64 + lane) * SLOT;
     if (kw == 1) {
 #pragma unroll
       for (int c = 0; c < NB; ++c)
@@ -536,52 +570,144 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) 
       xs[NB * 16 + 1] = l_run;
     }
     __syncthreads();
-    if (kw == 1) return;
-    const float m1 = xs[NB * 16], l1 = xs[NB * 16 + 1];
-    const float mm = fmaxf(m_run, m1);
-    const float mref = mm == kNegInf ? 0.f : mm;
-    const float a0 = __builtin_amdgcn_exp2f(m_run - mref), a1 = __builtin_amdgcn_exp2f(m1 - mref);
+    if (kw == 0) {
+      const float m1 = xs[NB * 16], l1 = xs[NB * 16 + 1];
+      const float mm = fmaxf(m_run, m1);
+      const float mref = mm == kNegInf ? 0.f : mm;
+      const float a0 = __builtin_amdgcn_exp2f(m_run - mref), a1 = __builtin_amdgcn_exp2f(m1 - mref);
 #pragma unroll
-    for (int c = 0; c < NB; ++c)
+      for (int c = 0; c < NB; ++c)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) o[c][j] = o[c][j] * a0 + xs[c * 16 + j] * a1;
-    l_run = l_run * a0 + l1 * a1;
-    m_run = mm;
+        for (int j = 0; j < 16; ++j) o[c][j] = o[c][j] * a0 + xs[c * 16 + j] * a1;
+      l_run = l_run * a0 + l1 * a1;
+      m_run = mm;
+    }
   }
   const float l_tot = xhalf_sum(l_run);
-  if (!row_in) return;
-
   // Register j of o[c] holds dim 32*c + 8*(j/4) + 4*h + j%4 of this row.
-  if (w.nsplit == 1) {
-    const bool valid = myvis != 0ull;
-    const float inv = valid ? 1.f / l_tot : 0.f;
-    uint16_t* orow = static_cast<uint16_t*>(a.out) +
-                     ((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D;
+  if (row_in && (KW == 1 || kw == 0)) {
+    if (w.final) {
+      const bool valid = myvis != 0ull;
+      const float inv = valid ? 1.f / l_tot : 0.f;
+      uint16_t* orow = static_cast<uint16_t*>(a.out) +
+                       ((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D;
 #pragma unroll
-    for (int c = 0; c < NB; ++c)
+      for (int c = 0; c < NB; ++c)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const u32x2 v = {pack2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
-                         pack2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
-        *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * q + 4 * h) = v;
+        for (int q = 0; q < 4; ++q) {
+          const u32x2 v = {pack2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
+                           pack2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
+          *reinterpret_cast<u32x2*>(orow + 32 * c + 8 * q + 4 * h) = v;
+        }
+      if (a.lse && h == 0)
+        a.lse[(static_cast<int64_t>(w.b) * a.hq + hq) * a.n_new + t] =
+            valid ? (m_run + __log2f(l_tot)) * kLn2 : kNegInf;
+    } else {
+      float* part = w.part;
+      float* prow = part + rowl * D;
+#pragma unroll
+      for (int c = 0; c < NB; ++c)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v = {o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
+          *reinterpret_cast<f32x4*>(prow + 32 * c + 8 * q + 4 * h) = v;
+        }
+      if (h == 0) {
+        part[a.rows_pb * D + rowl] = m_run;
+        part[a.rows_pb * D + a.rows_pb + rowl] = l_tot;
       }
-    if (a.lse && h == 0)
-      a.lse[(static_cast<int64_t>(w.b) * a.hq + hq) * a.n_new + t] =
-          valid ? (m_run + __log2f(l_tot)) * kLn2 : kNegInf;
-    return;
-  }
-  float* part = partial_base(a, w, D);
-  float* prow = part + rowl * D;
-#pragma unroll
-  for (int c = 0; c < NB; ++c)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const f32x4 v = {o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
-      *reinterpret_cast<f32x4*>(prow + 32 * c + 8 * q + 4 * h) = v;
     }
-  if (h == 0) {
-    part[a.rows_pb * D + rowl] = m_run;
-    part[a.rows_pb * D + a.rows_pb + rowl] = l_tot;
+  }
+}
+
+// Chunked decomposition: one work-group per (prefix chunk, KV head x row
+// block, sequence).
+template <int D, int RW, int KW, bool PAGED>
+__global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
+  Work w;
+  if (!setup_work(a, w, D)) return;
+  attend_segment<D, RW, KW, PAGED>(a, w);
+}
+
+// Stream decomposition, for large and ragged batches.  The tiles of all
+// pairs form one sequence: pair q = kvh * row_blocks + rb of sequence b owns
+// tp_b consecutive tiles (its prefix tiles, then the new-slot tile) starting
+// at seq0[b] + q * tp_b.  Work-group g of G takes tiles [g*T/G, (g+1)*T/G),
+// so every group gets the same number of tiles however ragged the prefixes
+// are (G = min(grid, T), so no range is empty); it attends over each pair's part of its range in turn.  A part that
+// covers a whole pair writes the output; the others write partials to the
+// group's two slots (0: the part at the start of its range, 1: the part at
+// its end), which the merge kernel locates from the same arithmetic.
+// seq0[0..batch] (int64) in LDS, and (group 0) in the workspace for the merge.
+__device__ inline void stream_offsets(const AttnArgs& a, int64_t* seq0) {
+  const int tid = threadIdx.x;
+  const int pps = a.hkv * a.row_blocks;
+  if (tid < kMaxStreamBatch) {
+    int64_t v = 0;
+    if (tid < a.batch) {
+      const int plen = min(max(a.prefix_lens[tid], 0), a.max_prefix);
+      v = static_cast<int64_t>(pps) * ((plen + kTile - 1) / kTile + 1);
+    }
+    seq0[tid + 1] = v;
+  }
+  if (tid == 0) seq0[0] = 0;
+  __syncthreads();
+  for (int off = 1; off < kMaxStreamBatch; off <<= 1) {   // inclusive scan of seq0[1..]
+    const int64_t v = (tid < kMaxStreamBatch && tid >= off) ? seq0[1 + tid - off] : 0;
+    __syncthreads();
+    if (tid < kMaxStreamBatch) seq0[1 + tid] += v;
+    __syncthreads();
+  }
+}
+
+template <int D, int RW, int KW, bool PAGED>
+__global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_stream(AttnArgs a) {
+  __shared__ int64_t seq0[kMaxStreamBatch + 1];
+  stream_offsets(a, seq0);
+  // Every lane computes the same values from LDS; readfirstlane makes that
+  // uniformity visible to the compiler (scalar registers, scalar branches).
+  auto uni = [](int64_t v) {
+    const uint32_t h = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v >> 32)));
+    const uint32_t l = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v & 0xffffffff)));
+    return static_cast<int64_t>((static_cast<uint64_t>(h) << 32) | l);
+  };
+  const int pps = a.hkv * a.row_blocks;
+  const int64_t T = uni(seq0[a.batch]);
+  const int g = blockIdx.x;
+  if (g == 0)
+    for (int i = threadIdx.x; i <= a.batch; i += blockDim.x) a.stream_seq0[i] = seq0[i];
+  // With fewer tiles than groups only the first T groups work, so that every
+  // working group's range is non-empty (the merge reads a slot of each).
+  const int G = static_cast<int>(min<int64_t>(gridDim.x, T));
+  if (g >= G) return;
+  const int64_t lo = static_cast<int64_t>(g) * T / G, hi = static_cast<int64_t>(g + 1) * T / G;
+  for (int64_t x = lo; x < hi;) {
+    int b = 0;                                 // the sequence holding tile x
+    for (int step = kMaxStreamBatch; step > 0; step >>= 1)
+      if (b + step < a.batch && uni(seq0[b + step]) <= x) b += step;
+    const int64_t s_b = uni(seq0[b]);
+    const int64_t tp = (uni(seq0[b + 1]) - s_b) / pps;
+    const int64_t local = x - s_b;
+    const int q = static_cast<int>(local / tp);
+    const int t0 = static_cast<int>(local % tp);
+    const int t1 = static_cast<int>(min(tp, t0 + (hi - x)));
+    const int ntp = static_cast<int>(tp) - 1;
+    Work w;
+    w.b = b;
+    w.kvh = q / a.row_blocks;
+    w.rb = q % a.row_blocks;
+    w.split = 0;
+    w.nsplit = 0;
+    w.plen = min(max(a.prefix_lens[b], 0), a.max_prefix);
+    w.gamma = min(max(a.num_ref[b], 0), a.L);
+    w.kbeg = min(t0, ntp) * kTile;
+    w.kend = min(min(t1, ntp) * kTile, w.plen);
+    w.has_new = t1 == tp;
+    w.final = t0 == 0 && t1 == tp;
+    w.part = a.part + (static_cast<int64_t>(g) * 2 + (x == lo ? 0 : 1)) *
+                          static_cast<int64_t>(a.rows_pb) * (D + 2);
+    attend_segment<D, RW, KW, PAGED>(a, w);
+    x += t1 - t0;
   }
 }
 
@@ -602,7 +728,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
   __shared__ uint64_t vis[kMaxNew];
 
   Work w;
-  if (!setup_work(a, w)) return;
+  if (!setup_work(a, w, D)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
   build_visibility<NT / 64>(vis, step_row[min(lane, a.B - 1)], w.gamma, a.B, a.n_new, wave, lane);
@@ -624,7 +750,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 
   const float sl2 = a.scale_log2;
   const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + TK - 1) / TK : 0;
-  const int ntn = w.split == 0 ? (a.n_new + TK - 1) / TK : 0;
+  const int ntn = w.has_new ? (a.n_new + TK - 1) / TK : 0;
   const int j = lane & 15, qtr = lane >> 4;
   for (int it = 0; it < ntp + ntn; ++it) {
     const bool is_new = it >= ntp;
@@ -688,7 +814,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
   }
   __syncthreads();
 
-  if (w.nsplit == 1) {
+  if (w.final) {
     for (int r = 0; r < RPW; ++r) {
       const int rowl = wave * RPW + r;
       const int m = w.rb * a.rows_pb + rowl;
@@ -705,7 +831,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
     }
     return;
   }
-  float* part = partial_base(a, w, D);
+  float* part = w.part;
   for (int idx = tid; idx < 32 * D; idx += NT) part[idx] = so[idx];
   if (tid < 32) {
     part[a.rows_pb * D + tid] = sm[tid];
@@ -718,10 +844,15 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 // block, sequence); one thread per (row, 4 dims).  Sequences whose prefix fits
 // one chunk were finished by the attention kernel and are skipped.
 // ----------------------------------------------------------------------------
-template <int D, typename OutT>
+// Merge of the partials of each pair.  Chunked decomposition: the pair's
+// nsplit chunk partials.  Stream decomposition: the partials of the groups
+// g_first..g_last whose tile ranges meet the pair (slot 1 of g_first when the
+// pair starts inside its range, slot 0 otherwise); a pair inside one group's
+// range was written whole by that group.
+template <int D, typename OutT, bool STREAM>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int D4 = D / 4;
-  constexpr int SB = 8;                        // splits merged per round of loads
+  constexpr int SB = 16;                       // splits merged per round of loads
   // A zero the compiler cannot see through: keeps the per-sequence reads
   // vector loads issued with the others instead of late scalar loads.
   int lane_zero;
@@ -739,29 +870,53 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   // First round of loads, none waiting on another.  Indices are clamped so
   // every load is in bounds; split blocks past this sequence's count (stale
   // workspace) are loaded but never used.
-  const int plen_raw = a.prefix_lens[b + lane_zero];
   const int nref = a.num_ref[b + lane_zero];
   const int step = a.step_map[static_cast<int64_t>(b) * a.B + min(t, a.B - 1)];
-  const int64_t pair = (static_cast<int64_t>(b) * a.hkv + kvh) * a.row_blocks + rb;
   const int64_t pstride = static_cast<int64_t>(a.rows_pb) * (D + 2);
-  const float* base = a.part + pair * a.splits * pstride;
   const int mo = a.rows_pb * D;
+  int nsplit;
+  const float* base = a.part;
+  int g_first = 0, G = 1;
+  int64_t start = 0, T = 1;
+  if constexpr (STREAM) {
+    const int64_t sb = a.stream_seq0[b + lane_zero], se = a.stream_seq0[b + 1 + lane_zero];
+    T = a.stream_seq0[a.batch + lane_zero];
+    G = static_cast<int>(min<int64_t>(a.stream_groups, T));   // the working groups
+    const int64_t tp = (se - sb) / (a.hkv * a.row_blocks);
+    start = sb + static_cast<int64_t>(kvh * a.row_blocks + rb) * tp;
+    // owner(x) = the group g with g*T/G <= x < (g+1)*T/G
+    g_first = static_cast<int>(((start + 1) * G - 1) / T);
+    const int g_last = static_cast<int>(((start + tp) * G - 1) / T);
+    nsplit = g_last - g_first + 1;
+  } else {
+    const int plen = min(max(a.prefix_lens[b + lane_zero], 0), a.max_prefix);
+    nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
+    base += ((static_cast<int64_t>(b) * a.hkv + kvh) * a.row_blocks + rb) * a.splits * pstride;
+  }
+  auto part_of = [&](int s) -> const float* {
+    if constexpr (STREAM) {
+      s = min(s, nsplit - 1);
+      const int g = g_first + s;
+      const int slot = (s == 0 && static_cast<int64_t>(g) * T / G < start) ? 1 : 0;
+      return base + (static_cast<int64_t>(g) * 2 + slot) * pstride;
+    } else {
+      return base + min(s, a.splits - 1) * pstride;
+    }
+  };
   float mv[SB], lv[SB];
   f32x4 ov[SB];
   auto load_round = [&](int s0) {
 #pragma unroll
     for (int s = 0; s < SB; ++s) {
-      const float* ps = base + min(s0 + s, a.splits - 1) * pstride;
+      const float* ps = part_of(s0 + s);
       mv[s] = ps[mo + rl];
       lv[s] = ps[mo + a.rows_pb + rl];
       ov[s] = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
     }
   };
-  load_round(0);
-
-  const int plen = min(max(plen_raw, 0), a.max_prefix);
-  const int nsplit = plen > 0 ? (plen + a.chunk - 1) / a.chunk : 1;
+  if (!STREAM) load_round(0);                  // chunked: before the split count is known
   if (nsplit <= 1) return;
+  if (STREAM) load_round(0);
   const int gamma = min(max(nref, 0), a.L);
   // A row is padding iff it sees no new slot (a non-padded row always sees itself).
   const bool valid = t < a.B ? step >= 0 : (t - a.B) < gamma;
@@ -804,8 +959,16 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
 }
 
 template <int D, bool PAGED>
-void launch_bf16(int row_waves, dim3 grid, const AttnArgs& a, hipStream_t st) {
-  switch (row_waves) {
+void launch_bf16(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st) {
+  if (p.stream) {
+    const dim3 sg(p.stream_groups);
+    switch (p.row_waves) {
+      case 2: hipLaunchKernelGGL((attn_bf16_stream<D, 2, 2, PAGED>), sg, dim3(256), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_bf16_stream<D, 4, 2, PAGED>), sg, dim3(512), 0, st, a); break;
+    }
+    return;
+  }
+  switch (p.row_waves) {
     case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
     case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
@@ -826,28 +989,31 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const bool paged = d.page_size > 0;
   if (d.dtype == SIMSD_BF16) {
     if (d.head_dim == 128) {
-      if (paged) launch_bf16<128, true>(p.row_waves, grid, a, st);
-      else launch_bf16<128, false>(p.row_waves, grid, a, st);
+      if (paged) launch_bf16<128, true>(p, grid, a, st);
+      else launch_bf16<128, false>(p, grid, a, st);
     } else {
-      if (paged) launch_bf16<64, true>(p.row_waves, grid, a, st);
-      else launch_bf16<64, false>(p.row_waves, grid, a, st);
+      if (paged) launch_bf16<64, true>(p, grid, a, st);
+      else launch_bf16<64, false>(p, grid, a, st);
     }
   } else {
     if (d.head_dim == 128) launch_f32<128>(paged, grid, a, st);
     else launch_f32<64>(paged, grid, a, st);
   }
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.splits <= 1) return e;
+  if (e != hipSuccess || (p.splits <= 1 && !p.stream)) return e;
   // Threads for the packed rows only (the last row block may be partial).
   const int per_block = (std::min(p.rows_pb, p.rows) * d.head_dim / 4 + 255) / 256;
   const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
   const bool bf16 = d.dtype == SIMSD_BF16;
-  if (d.head_dim == 128) {
-    if (bf16) hipLaunchKernelGGL((merge_kernel<128, uint16_t>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<128, float>), mgrid, dim3(256), 0, st, a);
+  if (p.stream) {
+    if (d.head_dim == 128) hipLaunchKernelGGL((merge_kernel<128, uint16_t, true>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, uint16_t, true>), mgrid, dim3(256), 0, st, a);
+  } else if (d.head_dim == 128) {
+    if (bf16) hipLaunchKernelGGL((merge_kernel<128, uint16_t, false>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<128, float, false>), mgrid, dim3(256), 0, st, a);
   } else {
-    if (bf16) hipLaunchKernelGGL((merge_kernel<64, uint16_t>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, float>), mgrid, dim3(256), 0, st, a);
+    if (bf16) hipLaunchKernelGGL((merge_kernel<64, uint16_t, false>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, float, false>), mgrid, dim3(256), 0, st, a);
   }
   return hipGetLastError();
 }

@@ -22,9 +22,11 @@ struct AttnArgs {
   void* out;
   float* lse;
   float* part;        // split partials (workspace), or null when splits == 1
+  int64_t* stream_seq0; // stream decomposition: per-sequence tile offsets (workspace)
   int64_t cs_seq, cs_tok, cs_head;
-  int hq, hkv, group, B, L, n_new, rows, rows_pb, row_blocks;
+  int batch, hq, hkv, group, B, L, n_new, rows, rows_pb, row_blocks;
   int page_size, max_pages, chunk, splits, max_prefix;
+  int stream_groups;  // stream decomposition: work-groups (0 = chunked decomposition)
   float scale_log2;
 };
 

@@ -48,8 +48,9 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   if (d->page_size > 0 && d->max_pages_per_seq < ceil_div(d->max_prefix_len, d->page_size))
     return fail(SIMSD_ERR_BAD_SHAPE,
                 "attention: max_pages_per_seq < ceil(max_prefix_len / page_size)");
-  if (d->kv_chunk < 0 || d->kv_chunk % kTile != 0)
-    return fail(SIMSD_ERR_BAD_SHAPE, "attention: kv_chunk must be 0 or a multiple of 64");
+  if (d->kv_chunk < kStreamChunk || (d->kv_chunk > 0 && d->kv_chunk % kTile != 0))
+    return fail(SIMSD_ERR_BAD_SHAPE,
+                "attention: kv_chunk must be -1 (stream), 0 (auto) or a multiple of 64");
   const int eb = elem_bytes(d->dtype);
   const int64_t strides[3] = {d->cache_stride_seq, d->cache_stride_token, d->cache_stride_head};
   for (int64_t s : strides) {
@@ -98,6 +99,29 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   if (r.splits > 65535 * 1024) return fail(SIMSD_ERR_BAD_SHAPE, "attention: too many splits");
   r.part_floats = static_cast<size_t>(r.rows_pb) * (d->head_dim + 2);
   r.workspace = r.splits > 1 ? static_cast<size_t>(r.pairs) * r.splits * r.part_floats * 4 : 0;
+  // Large bf16 problems take the stream decomposition: one work-group per
+  // resident slot, each with an equal share of all tiles (ragged prefixes do
+  // not unbalance it).  It is chosen when the chunked grid would take more than
+  // one round of resident groups (where ragged prefixes leave slots idle) and
+  // there are at least 8 tiles per group; kv_chunk -1 asks for it at any size.  Workspace: two partial slots per group, then the
+  // per-sequence tile offsets.  (Row blocks of up to 128 rows; the 8-wave
+  // 256-row group keeps the chunks.)
+  const bool can_stream = d->dtype == SIMSD_BF16 && d->batch <= kMaxStreamBatch &&
+                          r.row_waves <= 4;
+  if (d->kv_chunk == kStreamChunk && !can_stream)
+    return fail(SIMSD_ERR_UNSUPPORTED,
+                "attention: kv_chunk -1 (stream) needs bf16, at most 128 packed rows "
+                "(Hq/Hkv * (B + L)) and batch <= 256");
+  if (can_stream && d->kv_chunk <= 0) {
+    const int64_t groups = r.waves >= 8 ? kCUs : 2 * kCUs;
+    const int64_t tiles = r.pairs * (ceil_div(d->max_prefix_len, kTile) + 1);
+    if (d->kv_chunk == kStreamChunk || (tiles >= 8 * groups && r.pairs * r.splits > groups)) {
+      r.stream = true;
+      r.stream_groups = static_cast<int>(groups);
+      r.workspace = static_cast<size_t>(groups) * 2 * r.part_floats * 4 +
+                    static_cast<size_t>(kMaxStreamBatch + 1) * 8;
+    }
+  }
   const float scale = d->scale > 0.f ? d->scale : 1.0f / std::sqrt(static_cast<float>(d->head_dim));
   r.scale_log2 = scale * 1.4426950408889634f;
   *p = r;

@@ -14,7 +14,9 @@ constexpr int kTile = 64;            // keys per attention tile
 constexpr int kMaxNew = 64;          // B + L limit (one 64-bit visibility word per row)
 constexpr int kMaxGroup = 16;        // Hq / Hkv limit
 constexpr int kCUs = 256;            // compute units of an MI355X
-constexpr int kMinAutoChunk = 128;   // shortest automatic prefix chunk (keys)
+constexpr int kStreamChunk = -1;    // kv_chunk value that asks for the stream decomposition
+constexpr int kMaxStreamBatch = 256;  // stream decomposition: largest batch
+constexpr int kMinAutoChunk = 64;   // shortest automatic prefix chunk (keys)
 constexpr int kMaxAutoChunk = 8192;  // longest automatic prefix chunk (keys)
 constexpr int kAcceptThreads = 256;  // threads of the vocabulary-scan work-group
 constexpr int kAcceptTarget = 2048;  // scan work-groups the chunk heuristic aims for
@@ -29,6 +31,8 @@ struct AttnPlan {
   int row_blocks = 0;   // ceil(rows / rows_pb)
   int chunk = 0;        // prefix keys per split
   int splits = 0;       // grid.x: ceil(max_prefix_len / chunk), >= 1
+  bool stream = false;  // bf16: stream decomposition (equal tile ranges per work-group)
+  int stream_groups = 0;
   int64_t pairs = 0;    // batch * Hkv * row_blocks
   size_t part_floats = 0;   // floats per split partial: rows_pb * (head_dim + 2)
   size_t workspace = 0;     // total bytes

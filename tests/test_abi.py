@@ -80,6 +80,12 @@ def test_workspace_sizes_follow_the_plan():
     assert binding.attention_workspace_size(cfg_desc(1, kv_chunk=64)) == 0
     assert binding.attention_workspace_size(cfg_desc(2)) > 0
     assert binding.attention_workspace_size(cfg_desc(1, head_dim=96)) == 0   # invalid -> 0
+    # stream decomposition (kv_chunk -1): two partial slots per resident group
+    # plus 257 int64 sequence offsets; config 2 packs 128 rows -> 8 waves, 256 groups
+    assert binding.attention_workspace_size(cfg_desc(2, kv_chunk=-1)) == \
+        256 * 2 * 128 * 130 * 4 + 257 * 8
+    assert binding.attention_workspace_size(cfg_desc(2, kv_chunk=-1, dtype=binding.SIMSD_F32)) == 0
+    assert binding.attention_workspace_size(cfg_desc(4, kv_chunk=-1)) == 0   # 256 rows: no stream
     acc = AcceptDesc(batch=16, block_size=32, max_ref=32, vocab=151936, chunks_per_row=0,
                      logits_dtype=binding.SIMSD_BF16)
     # 512 rows -> 4 chunks per row; 16-byte partials
@@ -105,7 +111,7 @@ def call_attention(desc, **over):
     ("head_dim", 96, 3), ("head_dim", 256, 3), ("num_q_heads", 6, 2), ("num_kv_heads", 0, 2),
     ("num_q_heads", 136, 3), ("block_size", 0, 2), ("max_ref", 5, 2), ("block_size", 40, 2),
     ("batch", 0, 2), ("batch", 70000, 2), ("max_prefix_len", -1, 2), ("kv_chunk", 100, 2),
-    ("kv_chunk", -64, 2), ("page_size", -2, 2), ("cache_stride_token", 12, 4),
+    ("kv_chunk", -64, 2), ("kv_chunk", -2, 2), ("page_size", -2, 2), ("cache_stride_token", 12, 4),
     ("cache_stride_head", -8, 2), ("scale", -1.0, 2), ("scale", float("inf"), 2),
     ("dtype", 7, 3),
 ])

@@ -72,6 +72,12 @@ MIXED = [
     ("bf16", 128, 16, 2, 32, 32, (100, 400), 16, 64, 8),
     ("bf16", 64, 8, 2, 16, 16, (100, 300), 16, 64, 13),     # 128 rows: 4 row waves x 2
     ("bf16", 128, 12, 3, 24, 8, (0, 700), 32, 128, 14),     # 128 rows, paged, tail tiles
+    # stream decomposition at small sizes: fewer tiles than groups (one-tile
+    # ranges, many partials per pair), ragged and empty prefixes, paged
+    ("bf16", 128, 8, 2, 8, 8, (0, 300), 0, -1, 15),
+    ("bf16", 64, 8, 2, 16, 16, (100, 3000), 16, -1, 16),
+    ("bf16", 128, 4, 4, 4, 4, (0, 9000), 0, -1, 17),
+    ("bf16", 128, 12, 3, 24, 8, (0, 2500), 32, -1, 18),
     ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
     ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
     ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
@@ -107,7 +113,7 @@ def test_split_count_invariance_and_determinism():
     d = DeviceInputs(inp)
     ref_out, ref_lse = oracle.verify_attention(inp)
     outs = []
-    for chunk in (64, 192, 1024, 0, 0):
+    for chunk in (64, 192, 1024, -1, 0, 0):
         out, lse = run_attention(d, chunk)
         check_attention(out, lse, ref_out, ref_lse, "bf16")
         outs.append((out, lse))
