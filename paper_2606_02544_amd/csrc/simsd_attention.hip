@@ -387,6 +387,10 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
   }
   Ring kv;
   kv.init(a, w, wave, lane, s_pg);
+  // Every load the compiler knows of (Q, the step map, page ids) completes
+  // before the tile loads start: the compiler cannot see those, and a wait
+  // of its own after them would wait for the whole ring.
+  __builtin_amdgcn_s_waitcnt(0);
   if (PAGED) __syncthreads();                  // staged page ids
 
   const int ntp = w.kend > w.kbeg ? (w.kend - w.kbeg + kTile - 1) / kTile : 0;
@@ -401,7 +405,7 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
     if (j < nt) kv.issue(ring0 + j * kSlotBytes, tile_k0(j), j == ntp, w.kend, s_pg);
 
   build_visibility<NW>(vis, lane_step, w.gamma, a.B, a.n_new, wave, lane);
-  __syncthreads();                             // visibility words; every load above has landed
+  __syncthreads();                             // visibility words
   const uint64_t myvis = row_in ? vis[t] : 0ull;
 
   f32x16 o[NB];
@@ -849,10 +853,11 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 // g_first..g_last whose tile ranges meet the pair (slot 1 of g_first when the
 // pair starts inside its range, slot 0 otherwise); a pair inside one group's
 // range was written whole by that group.
-template <int D, typename OutT, bool STREAM>
+// SB partials are loaded per round (indices clamped, so a round always loads
+// SB); the launcher takes SB near the split count.
+template <int D, typename OutT, bool STREAM, int SB>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   constexpr int D4 = D / 4;
-  constexpr int SB = 16;                       // splits merged per round of loads
   // A zero the compiler cannot see through: keeps the per-sequence reads
   // vector loads issued with the others instead of late scalar loads.
   int lane_zero;
@@ -975,6 +980,15 @@ void launch_bf16(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st
   }
 }
 
+// Chunked merge: loads per round near the split count.
+template <int D, typename OutT>
+void launch_merge(int splits, dim3 grid, const AttnArgs& a, hipStream_t st) {
+  if (splits <= 2) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 2>), grid, dim3(256), 0, st, a);
+  else if (splits <= 4) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 4>), grid, dim3(256), 0, st, a);
+  else if (splits <= 8) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 8>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((merge_kernel<D, OutT, false, 16>), grid, dim3(256), 0, st, a);
+}
+
 template <int D>
 void launch_f32(bool paged, dim3 grid, const AttnArgs& a, hipStream_t st) {
   if (paged) hipLaunchKernelGGL((attn_f32_kernel<D, true>), grid, dim3(256), 0, st, a);
@@ -1006,14 +1020,14 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
   const bool bf16 = d.dtype == SIMSD_BF16;
   if (p.stream) {
-    if (d.head_dim == 128) hipLaunchKernelGGL((merge_kernel<128, uint16_t, true>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, uint16_t, true>), mgrid, dim3(256), 0, st, a);
+    if (d.head_dim == 128) hipLaunchKernelGGL((merge_kernel<128, uint16_t, true, 8>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, uint16_t, true, 8>), mgrid, dim3(256), 0, st, a);
   } else if (d.head_dim == 128) {
-    if (bf16) hipLaunchKernelGGL((merge_kernel<128, uint16_t, false>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<128, float, false>), mgrid, dim3(256), 0, st, a);
+    if (bf16) launch_merge<128, uint16_t>(p.splits, mgrid, a, st);
+    else launch_merge<128, float>(p.splits, mgrid, a, st);
   } else {
-    if (bf16) hipLaunchKernelGGL((merge_kernel<64, uint16_t, false>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, float, false>), mgrid, dim3(256), 0, st, a);
+    if (bf16) launch_merge<64, uint16_t>(p.splits, mgrid, a, st);
+    else launch_merge<64, float>(p.splits, mgrid, a, st);
   }
   return hipGetLastError();
 }
