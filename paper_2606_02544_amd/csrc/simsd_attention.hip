@@ -248,7 +248,7 @@ struct KVRing {
   bool fast;              // full tiles take the uniform-base path
   const int32_t* bt;      // this sequence's block table row
 
-  __device__ __attribute__((always_inline)) void init(const AttnArgs& a, const Work& w, int wave_, int lane, int* s_pg) {
+  __device__ __attribute__((always_inline)) void init(const AttnArgs& a, const Work& w, int wave_, int lane, SIMSD_LDS int* s_pg) {
     wave = wave_;
     const int64_t hoff = static_cast<int64_t>(w.kvh) * a.cs_head * 2;
     kc = static_cast<const char*>(a.k_cache) + hoff;
@@ -287,15 +287,17 @@ struct KVRing {
   }
 
   // Byte offset of (key, element 0) from this head's cache base (general path).
-  __device__ __attribute__((always_inline)) int64_t key_offset(int key, const int* s_pg) const {
+  __device__ __attribute__((always_inline)) int64_t key_offset(int key, const SIMSD_LDS int* s_pg) const {
     if (!PAGED) return seqoff + static_cast<int64_t>(key) * tokb;
+    // (s_pg is typed as LDS so that the compiler cannot fold the two reads
+    // into one load through a generic pointer.)
     const int64_t page = lds_pages ? s_pg[key / P - pg_first] : bt[key / P];
     return page * pageb + static_cast<int64_t>(key % P) * tokb;
   }
 
   // Issue this wave's share of the tile starting at prefix key k0 (or of the
   // new-slot tile) into the ring slot at LDS byte address `slot`.
-  __device__ __attribute__((always_inline)) void issue(uint32_t slot, int k0, bool is_new, int kend, const int* s_pg) const {
+  __device__ __attribute__((always_inline)) void issue(uint32_t slot, int k0, bool is_new, int kend, const SIMSD_LDS int* s_pg) const {
     if (is_new) {
 #pragma unroll
       for (int i = 0; i < PERW; ++i) {
@@ -351,7 +353,8 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
   using Ring = KVRing<D, NW, PAGED>;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF][2][TILEB];   // [slot][K, V]
   __shared__ uint64_t vis[kMaxNew];
-  __shared__ int s_pg[PAGED ? kMaxChunkPages : 1];
+  __shared__ int s_pg_arr[PAGED ? kMaxChunkPages : 1];
+  SIMSD_LDS int* s_pg = (SIMSD_LDS int*)(&s_pg_arr[0]);
 
   __syncthreads();                             // the work-group's previous range is done with the LDS
   const int tid = threadIdx.x, lane = tid & 63;

@@ -19,7 +19,7 @@ constexpr int kMaxStreamBatch = 256;  // stream decomposition: largest batch
 constexpr int kMinAutoChunk = 64;   // shortest automatic prefix chunk (keys)
 constexpr int kMaxAutoChunk = 8192;  // longest automatic prefix chunk (keys)
 constexpr int kAcceptThreads = 256;  // threads of the vocabulary-scan work-group
-constexpr int kAcceptTarget = 2048;  // scan work-groups the chunk heuristic aims for
+constexpr int kAcceptTarget = 512;   // scan work-groups the chunk heuristic aims for
 
 struct AttnPlan {
   int group = 0;        // Hq / Hkv
