@@ -111,7 +111,8 @@ def call_attention(desc, **over):
     ("head_dim", 96, 3), ("head_dim", 256, 3), ("num_q_heads", 6, 2), ("num_kv_heads", 0, 2),
     ("num_q_heads", 136, 3), ("block_size", 0, 2), ("max_ref", 5, 2), ("block_size", 40, 2),
     ("batch", 0, 2), ("batch", 70000, 2), ("max_prefix_len", -1, 2), ("kv_chunk", 100, 2),
-    ("kv_chunk", -64, 2), ("kv_chunk", -2, 2), ("page_size", -2, 2), ("cache_stride_token", 12, 4),
+    ("kv_chunk", -64, 2), ("kv_chunk", -2, 2), ("page_size", -2, 2),
+    ("stream_f32", -1, 3), ("stream_batch", -1, 3), ("stream_rows", -1, 3), ("cache_stride_token", 12, 4),
     ("cache_stride_head", -8, 2), ("scale", -1.0, 2), ("scale", float("inf"), 2),
     ("dtype", 7, 3),
 ])
@@ -119,7 +120,16 @@ def test_attention_descriptor_errors(field, value, status):
     desc = cfg_desc(2)
     if field == "block_size" and value == 40:
         desc.max_ref = 30                  # B + L = 70 > 64
-    setattr(desc, field, value)
+    if field.startswith("stream_"):        # kv_chunk -1 outside what it supports
+        desc.kv_chunk = value
+        if field == "stream_f32":
+            desc.dtype = binding.SIMSD_F32
+        elif field == "stream_batch":
+            desc.batch = 257
+        else:
+            desc = cfg_desc(4, kv_chunk=value)       # 256 packed rows
+    else:
+        setattr(desc, field, value)
     st, msg = call_attention(desc, workspace=FAKE, ws_bytes=1 << 40)
     assert st == status, (st, msg)
     assert msg

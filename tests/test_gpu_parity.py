@@ -78,6 +78,7 @@ MIXED = [
     ("bf16", 64, 8, 2, 16, 16, (100, 3000), 16, -1, 16),
     ("bf16", 128, 4, 4, 4, 4, (0, 9000), 0, -1, 17),
     ("bf16", 128, 12, 3, 24, 8, (0, 2500), 32, -1, 18),
+    ("bf16", 64, 4, 2, 4, 4, (0, 0), 0, -1, 19),           # stream, new-slot tiles only
     ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
     ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
     ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
@@ -106,6 +107,21 @@ def test_max_new_slots_and_group():
                        head_dim=128, prefix=(200, 333), block_size=32, max_ref=32,
                        vocab=4096, qkv_std=0.25, step_mode="mixed")
     _full_parity(generate(cfg, seed=31, poison=True), kv_chunk=128)
+
+
+def test_stream_largest_batch():
+    """The stream decomposition at its largest batch (256 sequences): the
+    per-sequence tile offsets are scanned over all 256 entries; ragged
+    prefixes, paged cache."""
+    cfg = VerifyConfig(0, "stream256", "bf16", batch=256, num_q_heads=8, num_kv_heads=2,
+                       head_dim=128, prefix=(0, 300), block_size=8, max_ref=8, vocab=512,
+                       page_size=16, qkv_std=0.3, step_mode="mixed")
+    inp = generate(cfg, seed=41, poison=True)
+    d = DeviceInputs(inp)
+    ref_out, ref_lse = oracle.verify_attention(inp)
+    for chunk in (-1, 0):
+        out, lse = run_attention(d, chunk)
+        check_attention(out, lse, ref_out, ref_lse, "bf16")
 
 
 def test_split_count_invariance_and_determinism():
