@@ -8,12 +8,14 @@
 // stored in memory.
 //
 // Work decomposition: one work-group per (prefix chunk, KV head x row block,
-// sequence).  The G query heads of a KV head and all B+L new slots are packed
-// into the rows of one row block (GQA packing), so each K/V byte of the prefix
-// is read from HBM once per KV head.  When a sequence's prefix spans several
-// chunks, each chunk writes an unnormalised partial output with its running
-// max and sum, and a second kernel merges them; there is no device-wide fence
-// or counter in the streaming kernel.
+// sequence), or, for large ragged batches, one work-group per resident slot
+// taking an equal range of all tiles (the stream decomposition).  The G query
+// heads of a KV head and all B+L new slots are packed into the rows of one
+// row block (GQA packing), so each K/V byte of the prefix is read from HBM
+// once per KV head.  When a pair's keys are split over several work-groups,
+// each writes an unnormalised partial output with its running max and sum,
+// and a second kernel merges them; there is no device-wide fence or counter
+// in the streaming kernel.
 //
 // bf16 path: K and V tiles of 64 keys stream into a ring of LDS tile slots
 // with direct global->LDS loads issued up to three tiles ahead, so no
