@@ -79,6 +79,9 @@ MIXED = [
     ("bf16", 128, 4, 4, 4, 4, (0, 9000), 0, -1, 17),
     ("bf16", 128, 12, 3, 24, 8, (0, 2500), 32, -1, 18),
     ("bf16", 64, 4, 2, 4, 4, (0, 0), 0, -1, 19),           # stream, new-slot tiles only
+    ("bf16", 64, 16, 2, 8, 8, (0, 500), 8, -1, 20),        # stream, 128 rows, d 64, 8-token pages
+    ("bf16", 128, 16, 2, 4, 4, (0, 700), 64, 0, 21),       # pages of exactly one tile
+    ("bf16", 64, 4, 4, 8, 8, (0, 400), 4, 64, 22),         # 4-token pages (one page per 4 rows)
     ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
     ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
     ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
