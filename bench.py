@@ -85,11 +85,38 @@ def recorded_traffic(workload: str):
         return None
 
 
-def cpu_baseline(inp, seconds: float):
-    """The oracle (float64 numpy) on the same workload, repeated whole steps
-    until ``seconds`` have passed, or on a subset of (sequence, KV head) pairs
-    plus their sequences' accept rows when one step takes longer."""
+def cpu_baseline(inp, seconds: float, outputs=None):
+    """The oracle leg.  The oracle (float64 numpy) on the same workload,
+    repeated whole steps until ``seconds`` have passed, or on a subset of
+    (sequence, KV head) pairs plus their sequences' accept rows when one step
+    takes longer; then, given the GPU outputs, the parity check.  Returns
+    (baseline, parity or None)."""
     import oracle
+
+    def parity_check(inp, outputs):
+        """The GPU outputs of the last timed step against the oracle: attention on
+        the first and the last (sequence, KV head) pair, accept on every row."""
+        cfg = inp.cfg
+        dt = cfg.dtype
+        b = cfg.batch
+        o = outputs["out"].float().cpu().double().numpy()
+        l_ = outputs["lse"].cpu().double().numpy()
+        pairs = [(0, 0), (b - 1, cfg.num_kv_heads - 1)]
+        ro, rl = oracle.verify_attention(inp, pairs=pairs)
+        G = cfg.group
+        ok = True
+        for s_, h_ in pairs:
+            sl = slice(h_ * G, (h_ + 1) * G)
+            err = np.abs(o[s_, :, sl] - ro[s_, :, sl]).max(-1)
+            ref = np.abs(ro[s_, :, sl]).max(-1)
+            tol = 2e-2 * ref if dt == "bf16" else np.full_like(ref, 1e-5)
+            ok &= bool(np.all(err <= tol))
+            ok &= bool(np.all(np.abs(l_[s_, sl] - rl[s_, sl]) <= 1e-4 * np.maximum(1, np.abs(rl[s_, sl]))))
+        rt, _, _, ra = oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, dt)
+        ok &= bool(np.array_equal(outputs["tid"].cpu().numpy(), rt))
+        ok &= bool(np.array_equal(outputs["alen"].cpu().numpy(), ra))
+        return {"checked": f"attention pairs {pairs}, accept all rows", "ok": ok}
+
     from threadpoolctl import threadpool_info
     cfg = inp.cfg
     pairs = [(s, h) for s in range(cfg.batch) for h in range(cfg.num_kv_heads)]
@@ -122,8 +149,9 @@ def cpu_baseline(inp, seconds: float):
     else:
         sample = f"{steps} whole steps" + (f" + {done_pairs - steps * len(pairs)} pairs" if done_pairs > steps * len(pairs) else "")
     threads = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
-    return {"value": tokens / dt, "unit": "verified tokens/s", "cores": threads,
+    base = {"value": tokens / dt, "unit": "verified tokens/s", "cores": threads,
             "kind": "oracle", "sample": sample + f", {dt:.1f} s float64 numpy"}
+    return base, (parity_check(inp, outputs) if outputs is not None else None)
 
 
 def main():
@@ -136,7 +164,8 @@ def main():
                          "4 long-context, 5 ragged-paged)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-check", action="store_true")
+    ap.add_argument("--no-check", action="store_true",
+                    help="skip the parity check of the oracle leg")
     ap.add_argument("--rotate-mb", type=float, default=640.0,
                     help="cycle input copies until this many MB are touched per cycle")
     ap.add_argument("--kv-chunk", type=int, default=0)
@@ -307,26 +336,6 @@ def main():
     print(f"[bench] done: {elapsed / K * 1e3:.4f} ms/step (attention {attn_ms * 1e3:.2f} us, "
           f"accept {acc_ms * 1e3:.2f} us per launch)", file=sys.stderr, flush=True)
 
-    parity = None
-    if not args.no_check:
-        import oracle
-        o = out.float().cpu().double().numpy()
-        l_ = lse.cpu().double().numpy()
-        pairs = [(0, 0), (b - 1, cfg.num_kv_heads - 1)]
-        ro, rl = oracle.verify_attention(inp, pairs=pairs)
-        G = cfg.group
-        ok = True
-        for s_, h_ in pairs:
-            sl = slice(h_ * G, (h_ + 1) * G)
-            err = np.abs(o[s_, :, sl] - ro[s_, :, sl]).max(-1)
-            ref = np.abs(ro[s_, :, sl]).max(-1)
-            tol = 2e-2 * ref if dt == "bf16" else np.full_like(ref, 1e-5)
-            ok &= bool(np.all(err <= tol))
-            ok &= bool(np.all(np.abs(l_[s_, sl] - rl[s_, sl]) <= 1e-4 * np.maximum(1, np.abs(rl[s_, sl]))))
-        rt, _, _, ra = oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, dt)
-        ok &= bool(np.array_equal(tid.cpu().numpy(), rt)) and bool(np.array_equal(alen.cpu().numpy(), ra))
-        parity = {"checked": f"attention pairs {pairs}, accept all rows", "ok": ok}
-
     value = wl["verified"] * K / elapsed
     attn_gbs = wl["attn_bytes"] / (attn_ms * 1e-3) / 1e9
     traffic = recorded_traffic(cfg.name)
@@ -367,11 +376,13 @@ def main():
             "frac": attn_gbs / HBM_PEAK_GBS,
             "traffic": traffic,
         },
-        "parity": parity,
     }
     if not args.no_cpu_baseline:
+        # The oracle leg: its rate on the host, and (unless --no-check) the last
+        # timed step's outputs checked against it on sampled pairs.
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
+        outputs = None if args.no_check else dict(out=out, lse=lse, tid=tid, alen=alen)
+        line["cpu_baseline"], line["parity"] = cpu_baseline(inp, args.cpu_seconds, outputs)
     print(json.dumps(line), flush=True)
 
 
