@@ -13,9 +13,10 @@
 // heads of a KV head and all B+L new slots are packed into the rows of one
 // row block (GQA packing), so each K/V byte of the prefix is read from HBM
 // once per KV head.  When a pair's keys are split over several work-groups,
-// each writes an unnormalised partial output with its running max and sum,
-// and a second kernel merges them; there is no device-wide fence or counter
-// in the streaming kernel.
+// each writes a partial output with its running max and sum (bf16: the output
+// normalised by its own sum, in bf16; fp32: unnormalised, in fp32), and a
+// second kernel merges them; there is no device-wide fence or counter in the
+// streaming kernel.
 //
 // bf16 path: K and V tiles of 64 keys stream into a ring of LDS tile slots
 // with direct global->LDS loads issued up to three tiles ahead, so no
@@ -97,7 +98,7 @@ __device__ inline void build_visibility(uint64_t* vis, int step, int gamma, int 
 // One contiguous key range of one (sequence, KV head, row block) pair that a
 // work-group attends over: prefix keys [kbeg, kend), plus the new-slot tile
 // when has_new.  A range that covers the whole pair (final) writes the
-// normalised output; any other writes an unnormalised partial to `part`.
+// normalised output; any other writes a partial (output, max, sum) to `part`.
 struct Work {
   int split, kvh, rb, b, plen, nsplit, kbeg, kend, gamma;
   bool has_new, final;
@@ -612,14 +613,18 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
         a.lse[(static_cast<int64_t>(w.b) * a.hq + hq) * a.n_new + t] =
             valid ? (m_run + __log2f(l_tot)) * kLn2 : kNegInf;
     } else {
+      // bf16 partial: this range's output normalised by its own sum (so in
+      // the range of V), rounded to bf16; the max and the sum stay fp32.
       float* part = w.part;
-      float* prow = part + rowl * D;
+      uint16_t* prow = reinterpret_cast<uint16_t*>(part) + rowl * D;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
 #pragma unroll
       for (int c = 0; c < NB; ++c)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const f32x4 v = {o[c][4 * q], o[c][4 * q + 1], o[c][4 * q + 2], o[c][4 * q + 3]};
-          *reinterpret_cast<f32x4*>(prow + 32 * c + 8 * q + 4 * h) = v;
+          const u32x2 v = {pack2(o[c][4 * q] * inv, o[c][4 * q + 1] * inv),
+                           pack2(o[c][4 * q + 2] * inv, o[c][4 * q + 3] * inv)};
+          *reinterpret_cast<u32x2*>(prow + 32 * c + 8 * q + 4 * h) = v;
         }
       if (h == 0) {
         part[a.rows_pb * D + rowl] = m_run;
@@ -921,7 +926,13 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
       const float* ps = part_of(s0 + s);
       mv[s] = ps[mo + rl];
       lv[s] = ps[mo + a.rows_pb + rl];
-      ov[s] = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
+      if constexpr (sizeof(OutT) == 2) {       // bf16 partials, normalised by their sum
+        const u32x2 w2 = *reinterpret_cast<const u32x2*>(reinterpret_cast<const uint16_t*>(ps) + rl * D + d0);
+        ov[s] = f32x4{__uint_as_float(w2[0] << 16), __uint_as_float(w2[0] & 0xffff0000u),
+                      __uint_as_float(w2[1] << 16), __uint_as_float(w2[1] & 0xffff0000u)};
+      } else {
+        ov[s] = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
+      }
     }
   };
   if (!STREAM) load_round(0);                  // chunked: before the split count is known
@@ -949,7 +960,8 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
       if (s0 + s < nsplit) {
         const float wt = __builtin_amdgcn_exp2f(mv[s] - mn);
         lsum += wt * lv[s];
-        acc += wt * ov[s];
+        // bf16 partials hold O / l: their weight carries the sum.
+        acc += (sizeof(OutT) == 2 ? wt * lv[s] : wt) * ov[s];
       }
     }
     mt = mn;
