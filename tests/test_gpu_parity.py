@@ -143,6 +143,41 @@ def test_split_count_invariance_and_determinism():
         check_accept(run_accept(d, cpr), ref)
 
 
+def test_optional_outputs_null():
+    """lse, confidence and draft_prob are optional (NULL): the other outputs
+    are unchanged, with one split and with several (the merge kernel)."""
+    import ctypes
+    from paper_2606_02544_amd import binding
+    from gpu_util import dev_tensor
+    inp = generate(CONFIGS[3].replace(batch=2, prefix=700), seed=91, poison=True)
+    d = DeviceInputs(inp)
+    cfg = inp.cfg
+    for chunk in (1024, 128, -1):
+        ref_out, _ = run_attention(d, chunk)
+        out, lse = binding.verify_attention(
+            d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_table, d.prefix_lens,
+            d.step_map, d.num_ref, block_size=cfg.block_size, max_ref=cfg.max_ref,
+            max_prefix_len=cfg.max_prefix, page_size=cfg.page_size, kv_chunk=chunk,
+            want_lse=False)
+        torch.cuda.synchronize()
+        assert lse is None
+        np.testing.assert_array_equal(out.float().cpu().double().numpy(), ref_out)
+    t_ref, _, _, a_ref = run_accept(d)
+    b, B = cfg.batch, cfg.block_size
+    tid = torch.empty((b, B), dtype=torch.int32, device="cuda")
+    alen = torch.empty((b,), dtype=torch.int32, device="cuda")
+    desc = binding.accept_desc(d.logits, cfg.max_ref)
+    ws = torch.zeros(max(binding.accept_workspace_size(desc), 16), dtype=torch.uint8, device="cuda")
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    st = binding.lib().simsd_verify_accept(
+        ctypes.byref(desc), P(d.logits), P(d.draft_ids), P(d.step_map), P(d.num_ref), P(tid),
+        None, None, P(alen), P(ws), ws.numel(), None)
+    torch.cuda.synchronize()
+    assert st == 0, binding.lib().simsd_last_error()
+    np.testing.assert_array_equal(tid.cpu().numpy(), t_ref)
+    np.testing.assert_array_equal(alen.cpu().numpy(), a_ref)
+
+
 def test_workspace_reuse_many_launches():
     """Repeated launches sharing one workspace keep producing the same bits."""
     inp = generate(CONFIGS[2], seed=5)
