@@ -239,16 +239,17 @@ def test_accept_bench_shape_chunking():
         check_accept(run_accept(d, cpr), ref)
 
 
-def test_hip_graph_replays_match_eager():
+@pytest.mark.parametrize("kv_chunk", [128, -1])
+def test_hip_graph_replays_match_eager(kv_chunk):
     """Both entry points captured in one HIP graph (the benchmark's timing
-    mode): every replay, with eager work and synchronisation in between,
-    reproduces the eager outputs bit for bit."""
+    mode), chunked and stream decompositions: every replay, with eager work and
+    synchronisation in between, reproduces the eager outputs bit for bit."""
     from paper_2606_02544_amd import binding
     inp = generate(CONFIGS[3].replace(batch=2, prefix=700), seed=3, poison=True)
     d = DeviceInputs(inp)
     cfg = inp.cfg
     kw = dict(block_size=cfg.block_size, max_ref=cfg.max_ref, max_prefix_len=cfg.max_prefix,
-              kv_chunk=128)
+              kv_chunk=kv_chunk)
     args = (d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_table, d.prefix_lens,
             d.step_map, d.num_ref)
     eager_out, eager_lse = binding.verify_attention(*args, **kw)
