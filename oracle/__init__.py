@@ -9,7 +9,10 @@ A plain, slow, float64 numpy statement of what the GPU path computes:
                   slots] under that mask (Sec. 3.2, "Target Model Verification");
   * ``accept``    the greedy (temperature-0) form of the acceptance rule of
                   eq. 2: argmax with lowest-index ties, softmax confidence, the
-                  target probability of each draft and the accepted prefix length.
+                  target probability of each draft and the accepted prefix length;
+  * ``sampled``   the stochastic form of eq. 2 at temperature T: acceptance with
+                  probability min(1, p_theta/p_phi) from caller-supplied uniforms
+                  and the residual draw at the first rejection.
 
 Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may
 import this package.  The product path (the C-ABI library and its Python
@@ -22,6 +25,7 @@ from .widen import widen
 from .mask import slot_labels, new_slot_visibility, DATA, MASK
 from .attention import attend, verify_attention
 from .accept import verify_accept
+from .sampled import verify_accept_sampled
 
 __all__ = ["widen", "slot_labels", "new_slot_visibility", "DATA", "MASK", "attend",
-           "verify_attention", "verify_accept"]
+           "verify_attention", "verify_accept", "verify_accept_sampled"]

@@ -116,3 +116,56 @@ def test_accept_mutations_caught(monkeypatch):
         return int(np.flatnonzero(x == m)[0]), m, m + np.exp(x - m).sum()
     monkeypatch.setattr(oacc, "scan_row", no_log)
     assert not tacc.all_pins_pass()
+
+
+# ---- stochastic acceptance ----------------------------------------------------
+
+import test_oracle_sampled as tsmp
+from oracle import sampled as osmp
+
+
+def sampled_pins_ok():
+    try:
+        tsmp.test_first_draft_output_is_target_distribution(1.0)
+        tsmp.test_first_draft_output_is_target_distribution(0.6)
+        tsmp.test_second_draft_output_is_its_target_distribution()
+        tsmp.test_hand_example()
+        tsmp.test_empty_residual_draws_from_target()
+        tsmp.test_probabilities_match_softmax_and_gamma_zero()
+        tsmp.test_small_temperature_is_greedy()
+    except AssertionError:
+        return False
+    return True
+
+
+def _sampled_variant(monkeypatch, which):
+    if which == "inverted_ratio":
+        monkeypatch.setattr(osmp, "accept_draft", lambda u, pt, pd: u * pt < pd)
+    elif which == "unclamped_residual":
+        monkeypatch.setattr(osmp, "residual", lambda pt, pd: ((pt - pd), False))
+    elif which == "target_not_residual":
+        monkeypatch.setattr(osmp, "residual", lambda pt, pd: (pt.copy(), True))
+    elif which == "temperature_ignored":
+        real = osmp.softmax_t
+        monkeypatch.setattr(osmp, "softmax_t", lambda x, T: real(x, 1.0))
+    elif which == "row_by_draft_index":
+        monkeypatch.setattr(osmp, "rows_of_steps", lambda step_row, gamma: list(range(gamma)))
+    elif which == "draw_reuses_accept_uniform":
+        real = osmp.verify_accept_sampled
+
+        def wrong(logits, dl, drafts, step, nref, u, T, dtype):
+            u = np.array(u, np.float64, copy=True)
+            L = drafts.shape[1]
+            # the draw takes the uniform of the first draft instead of its own
+            u[:, L] = u[:, 0]
+            return real(logits, dl, drafts, step, nref, u, T, dtype)
+        monkeypatch.setattr(osmp, "verify_accept_sampled", wrong)
+
+
+@pytest.mark.parametrize("which", ["inverted_ratio", "unclamped_residual", "target_not_residual",
+                                   "temperature_ignored", "row_by_draft_index",
+                                   "draw_reuses_accept_uniform"])
+def test_sampled_mutation_caught(monkeypatch, which):
+    assert sampled_pins_ok()
+    _sampled_variant(monkeypatch, which)
+    assert not sampled_pins_ok()
