@@ -16,7 +16,10 @@
  *                           fly, never stored), GQA-packed, split over the prefix;
  *   simsd_verify_accept     vocabulary scan of the verification rows (argmax with
  *                           lowest-index ties, confidence, draft probability) and
- *                           the accepted-prefix length, i.e. eq. 2 at temperature 0.
+ *                           the accepted-prefix length, i.e. eq. 2 at temperature 0;
+ *   simsd_verify_accept_sampled  eq. 2 at temperature T: acceptance with
+ *                           probability min(1, p_theta/p_phi) and the residual
+ *                           draw at the first rejection.
  *
  * Conventions shared by both calls
  * --------------------------------
@@ -202,6 +205,47 @@ simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const void* logi
                                  const int32_t* num_ref, int32_t* target_ids,
                                  float* confidence, float* draft_prob, int32_t* accept_len,
                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Stochastic verification (eq. 2 at temperature T > 0, Sec. 3.2; the paper's
+ * experiments use T = 1, Sec. 4.1): the rule the greedy call is the T -> 0
+ * limit of.  With p_theta(r) = softmax(logits[b, k_r] / T) at the
+ * verification row k_r of draft r and p_phi(r) = softmax(draft_logits[b, r-1]
+ * / T), draft r is accepted iff u_r * p_phi(r)(D_r) < p_theta(r)(D_r), which
+ * for u_r ~ U[0, 1) happens with probability min(1, p_theta / p_phi).  The
+ * longest accepted prefix is kept; at the first rejected draft a+1 the target's
+ * token is drawn from the residual max(0, p_theta(a+1) - p_phi(a+1)) by
+ * inverse CDF in vocabulary order: the smallest x whose running weight exceeds
+ * w * (total weight), w = uniforms[b, L].  If the residual is zero everywhere
+ * the draw uses p_theta(a+1).  The random numbers are the caller's.
+ *
+ *   temperature  T, finite and > 0 (else SIMSD_ERR_BAD_SHAPE)
+ *   logits       [batch, B, V]  target logits; rows of steps 1..gamma_b are read
+ *   draft_logits [batch, L, V]  row r-1 = the drafter's logits when it proposed
+ *                               draft r (same dtype as logits, 16-byte aligned);
+ *                               rows r-1 < gamma_b are read.  NULL only if L = 0
+ *   draft_ids    [batch, L] int32
+ *   step_map, num_ref           as for simsd_verify_attention
+ *   uniforms     [batch, L + 1] float32 in [0, 1): u_1..u_L, then w
+ *   p_target     [batch, L] float32  p_theta(r)(D_r), 0 for an id outside
+ *                                    [0, V) and for r > gamma_b; or NULL
+ *   p_draft      [batch, L] float32  p_phi(r)(D_r), likewise; or NULL
+ *   accept_len   [batch] int32       accepted drafts, 0..gamma_b.  A draft id
+ *                                    outside [0, V) is a rejection.
+ *   correction   [batch] int32       token drawn at the first rejection, or -1
+ *                                    when every draft was accepted
+ * Probabilities and running sums are float32: the draw can differ from an
+ * exact one only where w * total falls within rounding of a boundary.
+ * The workspace must hold simsd_verify_accept_sampled_workspace_size() bytes.
+ */
+size_t simsd_verify_accept_sampled_workspace_size(const simsd_accept_desc* desc);
+simsd_status simsd_verify_accept_sampled(const simsd_accept_desc* desc, float temperature,
+                                         const void* logits, const void* draft_logits,
+                                         const int32_t* draft_ids, const int32_t* step_map,
+                                         const int32_t* num_ref, const float* uniforms,
+                                         float* p_target, float* p_draft, int32_t* accept_len,
+                                         int32_t* correction, void* workspace,
+                                         size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Host-only helpers (no GPU needed)                                          */

@@ -68,6 +68,11 @@ def lib() -> ctypes.CDLL:
         L.simsd_verify_accept.argtypes = [ctypes.POINTER(AcceptDesc)] + [_P] * 8 + \
             [_P, ctypes.c_size_t, _P]
         L.simsd_verify_accept.restype = ctypes.c_int
+        L.simsd_verify_accept_sampled_workspace_size.argtypes = [ctypes.POINTER(AcceptDesc)]
+        L.simsd_verify_accept_sampled_workspace_size.restype = ctypes.c_size_t
+        L.simsd_verify_accept_sampled.argtypes = [ctypes.POINTER(AcceptDesc), ctypes.c_float] + \
+            [_P] * 10 + [_P, ctypes.c_size_t, _P]
+        L.simsd_verify_accept_sampled.restype = ctypes.c_int
         L.simsd_validate_step_map.argtypes = [_I32P, _I32P, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32]
         L.simsd_validate_step_map.restype = ctypes.c_int
@@ -212,6 +217,40 @@ def verify_accept(logits, draft_ids, step_map, num_ref, *, chunks_per_row: int =
         _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
         _ptr(workspace), ws_bytes, _stream(stream)))
     return target_ids, confidence, draft_prob, accept_len
+
+
+def accept_sampled_workspace_size(desc: AcceptDesc) -> int:
+    return int(lib().simsd_verify_accept_sampled_workspace_size(ctypes.byref(desc)))
+
+
+def verify_accept_sampled(logits, draft_logits, draft_ids, step_map, num_ref, uniforms, *,
+                          temperature: float = 1.0, chunks_per_row: int = 0, p_target=None,
+                          p_draft=None, accept_len=None, correction=None, workspace=None,
+                          stream=None, desc: Optional[AcceptDesc] = None):
+    """simsd_verify_accept_sampled on torch tensors.
+    Returns (p_target, p_draft, accept_len, correction)."""
+    b, B, V = logits.shape
+    L = draft_ids.shape[1]
+    if desc is None:
+        desc = accept_desc(logits, L, chunks_per_row)
+    dev = logits.device
+    if p_target is None:
+        p_target = torch.empty((b, L), dtype=torch.float32, device=dev)
+    if p_draft is None:
+        p_draft = torch.empty((b, L), dtype=torch.float32, device=dev)
+    if accept_len is None:
+        accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
+    if correction is None:
+        correction = torch.empty((b,), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = WORKSPACES.get(dev, "accept_sampled", accept_sampled_workspace_size(desc))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().simsd_verify_accept_sampled(
+        ctypes.byref(desc), ctypes.c_float(temperature), _ptr(logits), _ptr(draft_logits),
+        _ptr(draft_ids), _ptr(step_map), _ptr(num_ref), _ptr(uniforms), _ptr(p_target),
+        _ptr(p_draft), _ptr(accept_len), _ptr(correction), _ptr(workspace), ws_bytes,
+        _stream(stream)))
+    return p_target, p_draft, accept_len, correction
 
 
 def validate_step_map(step_map, num_ref, max_ref: int):

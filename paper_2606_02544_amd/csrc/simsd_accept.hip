@@ -30,25 +30,26 @@ struct Best {
   float sm;  // sum of exp(x - mx)
 };
 
-__device__ inline Best combine(Best a, Best b) {
+// cl = log2(e) / T: the sums are of exp((x - max) / T).
+__device__ inline Best combine(Best a, Best b, float cl) {
   const float M = fmaxf(a.mx, b.mx);
   Best r;
   r.mx = M;
   r.ix = a.mx > b.mx ? a.ix : (b.mx > a.mx ? b.ix : min(a.ix, b.ix));
-  const float sa = a.mx == kNegInf ? 0.f : a.sm * __builtin_amdgcn_exp2f((a.mx - M) * kLog2e);
-  const float sb = b.mx == kNegInf ? 0.f : b.sm * __builtin_amdgcn_exp2f((b.mx - M) * kLog2e);
+  const float sa = a.mx == kNegInf ? 0.f : a.sm * __builtin_amdgcn_exp2f((a.mx - M) * cl);
+  const float sb = b.mx == kNegInf ? 0.f : b.sm * __builtin_amdgcn_exp2f((b.mx - M) * cl);
   r.sm = sa + sb;
   return r;
 }
 
-__device__ inline Best wave_reduce(Best v) {
+__device__ inline Best wave_reduce(Best v, float cl) {
 #pragma unroll
   for (int sh = 32; sh >= 1; sh >>= 1) {
     Best o;
     o.mx = __shfl_xor(v.mx, sh);
     o.ix = __shfl_xor(v.ix, sh);
     o.sm = __shfl_xor(v.sm, sh);
-    v = combine(v, o);
+    v = combine(v, o, cl);
   }
   return v;
 }
@@ -85,7 +86,7 @@ __device__ inline void load_vec(const void* row, int64_t v, float (&x)[VEC]) {
 
 // Scan vectors [v0, v1) of one row; returns this work-group's (max, index, sum).
 template <bool BF16, int VEC>
-__device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, Best* s_red) {
+__device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, float cl, Best* s_red) {
   float mx = kNegInf, sm = 0.f;
   int64_t vbest = -1;
   constexpr int U = 4;
@@ -100,13 +101,13 @@ __device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, Bes
 #pragma unroll
       for (int i = 1; i < VEC; ++i) vm = fmaxf(vm, x[u][i]);
       if (vm > mx) {
-        sm = mx == kNegInf ? 0.f : sm * __builtin_amdgcn_exp2f((mx - vm) * kLog2e);
+        sm = mx == kNegInf ? 0.f : sm * __builtin_amdgcn_exp2f((mx - vm) * cl);
         mx = vm;
         vbest = v + u * NT;
       }
-      const float off = mx * kLog2e;
+      const float off = mx * cl;
 #pragma unroll
-      for (int i = 0; i < VEC; ++i) sm += __builtin_amdgcn_exp2f(fmaf(x[u][i], kLog2e, -off));
+      for (int i = 0; i < VEC; ++i) sm += __builtin_amdgcn_exp2f(fmaf(x[u][i], cl, -off));
     }
   }
   for (; v < v1; v += NT) {
@@ -116,13 +117,13 @@ __device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, Bes
 #pragma unroll
     for (int i = 1; i < VEC; ++i) vm = fmaxf(vm, x[i]);
     if (vm > mx) {
-      sm = mx == kNegInf ? 0.f : sm * __builtin_amdgcn_exp2f((mx - vm) * kLog2e);
+      sm = mx == kNegInf ? 0.f : sm * __builtin_amdgcn_exp2f((mx - vm) * cl);
       mx = vm;
       vbest = v;
     }
-    const float off = mx * kLog2e;
+    const float off = mx * cl;
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) sm += __builtin_amdgcn_exp2f(fmaf(x[i], kLog2e, -off));
+    for (int i = 0; i < VEC; ++i) sm += __builtin_amdgcn_exp2f(fmaf(x[i], cl, -off));
   }
   Best me = {kNegInf, kNoIndex, 0.f};
   if (vbest >= 0) {
@@ -136,35 +137,46 @@ __device__ Best scan_chunk(const void* row, int64_t v0, int64_t v1, int tid, Bes
     me.ix = static_cast<int>(vbest * VEC + first);
     me.sm = sm;
   }
-  me = wave_reduce(me);
+  me = wave_reduce(me, cl);
   const int lane = tid & 63, wave = tid >> 6;
   if (lane == 0) s_red[wave] = me;
   __syncthreads();
   Best r = s_red[0];
-  for (int i = 1; i < NT / 64; ++i) r = combine(r, s_red[i]);
+  for (int i = 1; i < NT / 64; ++i) r = combine(r, s_red[i], cl);
   return r;
 }
 
 // One work-group per (vocabulary chunk, block slot, sequence): writes the
 // chunk's (max, lowest index, sum of exp) to the workspace.
-template <bool BF16, int VEC>
+// Greedy: row y < B is block slot y, scanned when its step is >= 1.  Sampled:
+// rows y < B are the verification rows (steps 1..gamma), and row B + r is the
+// drafter's logits for draft r + 1 (r < gamma).
+template <bool BF16, int VEC, bool SAMPLED>
 __global__ void __launch_bounds__(NT) scan_kernel(AcceptArgs a) {
   __shared__ Best s_red[NT / 64];
-  const int c = blockIdx.x, k = blockIdx.y, b = blockIdx.z;
-  const int64_t rowi = static_cast<int64_t>(b) * a.B + k;
-  if (a.step_map[rowi] < 1) return;          // committed or padding: not scanned
+  const int c = blockIdx.x, y = blockIdx.y, b = blockIdx.z;
   const int esz = BF16 ? 2 : 4;
-  const char* row = static_cast<const char*>(a.logits) + rowi * a.V * esz;
+  const char* row;
+  if (y < a.B) {
+    const int step = a.step_map[static_cast<int64_t>(b) * a.B + y];
+    if (step < 1) return;                    // committed or padding: not scanned
+    if (SAMPLED && step > min(max(a.num_ref[b], 0), a.L)) return;   // not drafted
+    row = static_cast<const char*>(a.logits) + (static_cast<int64_t>(b) * a.B + y) * a.V * esz;
+  } else {
+    const int r = y - a.B;
+    if (r >= min(max(a.num_ref[b], 0), a.L)) return;
+    row = static_cast<const char*>(a.draft_logits) + (static_cast<int64_t>(b) * a.L + r) * a.V * esz;
+  }
   const int64_t v0 = static_cast<int64_t>(c) * a.chunk_vecs;
   const int64_t v1 = min(a.nvec, v0 + a.chunk_vecs);
-  const Best r = scan_chunk<BF16, VEC>(row, v0, v1, threadIdx.x, s_red);
+  const Best r = scan_chunk<BF16, VEC>(row, v0, v1, threadIdx.x, a.cl, s_red);
   if (threadIdx.x == 0) {
     AcceptPartial pr;
     pr.mx = r.mx;
     pr.ix = r.ix;
     pr.sm = r.sm;
     pr.pad = 0;
-    a.part[rowi * a.cpr + c] = pr;
+    a.part[(static_cast<int64_t>(b) * a.rows + y) * a.cpr + c] = pr;
   }
 }
 
@@ -218,7 +230,7 @@ __device__ inline void merge_packed(const AcceptArgs& a, int wave, int lane, int
       o.mx = __shfl_xor(r.mx, sh);
       o.ix = __shfl_xor(r.ix, sh);
       o.sm = __shfl_xor(r.sm, sh);
-      r = combine(r, o);
+      r = combine(r, o, a.cl);
     }
     if (cc == 0 && kk < a.B) s_row[kk] = r;
   }
@@ -236,9 +248,9 @@ __device__ inline void merge_rows(const AcceptArgs& a, int wave, int lane,
 #pragma unroll
     for (int q = 0; q < PPL; ++q) {
       const AcceptPartial pr = buf[j * PPL + q];
-      if (lane + 64 * q < a.cpr) r = combine(r, Best{pr.mx, pr.ix, pr.sm});
+      if (lane + 64 * q < a.cpr) r = combine(r, Best{pr.mx, pr.ix, pr.sm}, a.cl);
     }
-    r = wave_reduce(r);
+    r = wave_reduce(r, a.cl);
     if (lane == 0) s_row[kk] = r;
   }
 }
@@ -254,7 +266,7 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
   const int b = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(b) * a.B;
-  const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.B * a.cpr;
+  const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.rows * a.cpr;
   const int esz = BF16 ? 2 : 4;
   const char* logits_b = static_cast<const char*>(a.logits) + static_cast<int64_t>(b) * a.B * a.V * esz;
 
@@ -303,9 +315,9 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
       Best rr = {kNegInf, kNoIndex, 0.f};
       for (int cc = lane; cc < a.cpr; cc += 64) {
         const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
-        rr = combine(rr, Best{pr.mx, pr.ix, pr.sm});
+        rr = combine(rr, Best{pr.mx, pr.ix, pr.sm}, a.cl);
       }
-      rr = wave_reduce(rr);
+      rr = wave_reduce(rr, a.cl);
       if (lane == 0) s_row[kk] = rr;
     }
   }
@@ -324,12 +336,217 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
     if (r < gamma) {
       rejected = kr < 0 || s_row[kr].ix != tok;
       if (kr >= 0 && tok >= 0 && tok < a.V)
-        p = __builtin_amdgcn_exp2f((x - s_row[kr].mx) * kLog2e) / s_row[kr].sm;
+        p = __builtin_amdgcn_exp2f((x - s_row[kr].mx) * a.cl) / s_row[kr].sm;
     }
     if (a.draft_prob && r < a.L) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = p;
     const unsigned long long rej = __ballot(rejected);
     if (lane == 0) a.accept_len[b] = rej ? __ffsll(static_cast<long long>(rej)) - 1 : gamma;
   }
+}
+
+// ---- Stochastic acceptance: eq. 2 at temperature T ---------------------------
+//
+// Draft r is accepted iff u_r * p_phi(D_r) < p_theta(D_r) (probability
+// min(1, p_theta / p_phi) for u_r ~ U[0, 1)), in draft order; the accepted
+// prefix ends at the first rejection, where the token is drawn from the
+// residual max(0, p_theta - p_phi) (or p_theta when that is empty everywhere)
+// by inverse CDF in vocabulary order with the uniform w = uniforms[b, L].
+// One work-group per sequence.  The draw reads the two rows twice: once for
+// per-wave totals (each wave owns a contiguous quarter of the vocabulary,
+// read in coalesced stripes), then, in the wave whose quarter holds the
+// target w * Z, stripe by stripe with a wave prefix sum until the running sum
+// passes it.
+template <bool BF16, int VEC>
+__global__ void __launch_bounds__(NT) finalize_sampled_kernel(AcceptArgs a) {
+  constexpr int NWV = NT / 64;
+  __shared__ Best s_row[2 * kMaxNew];        // [0, B): verification rows; B + r: draft row r
+  __shared__ int s_step[kMaxNew];
+  __shared__ int s_row_of_step[kMaxNew];
+  __shared__ float s_tot[2][NWV];            // per-wave sums: residual, p_theta
+  __shared__ int s_last[2][NWV];             // per-wave last index of positive weight
+  __shared__ int s_acc;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int esz = BF16 ? 2 : 4;
+  const int32_t* step_row = a.step_map + static_cast<int64_t>(b) * a.B;
+  const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.rows * a.cpr;
+  const float* urow = a.uniforms + static_cast<int64_t>(b) * (a.L + 1);
+
+  // First round of loads, none waiting on another (see finalize_kernel).
+  int lane_zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(lane_zero));
+  const int nref = a.num_ref[b + lane_zero];
+  const int step_t = step_row[min(tid, a.B - 1)];
+  int tok = -1;
+  if (a.L > 0) tok = a.draft_ids[static_cast<int64_t>(b) * a.L + min(lane, a.L - 1)];
+  const float u = urow[min(lane, a.L)];
+  const int gamma = min(max(nref, 0), a.L);
+  if (tid < a.B) s_step[tid] = step_t;
+  if (tid < kMaxNew) s_row_of_step[tid] = -1;
+  __syncthreads();
+  if (tid < a.B && step_t >= 1 && step_t <= gamma) s_row_of_step[step_t - 1] = tid;
+
+  // Merge the chunks of the rows the step reads (verification rows of steps
+  // 1..gamma, draft rows 0..gamma-1).
+  for (int kk = wave; kk < a.B + gamma; kk += NWV) {
+    if (kk < a.B && !(s_step[kk] >= 1 && s_step[kk] <= gamma)) continue;
+    Best rr = {kNegInf, kNoIndex, 0.f};
+    for (int cc = lane; cc < a.cpr; cc += 64) {
+      const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
+      rr = combine(rr, Best{pr.mx, pr.ix, pr.sm}, a.cl);
+    }
+    rr = wave_reduce(rr, a.cl);
+    if (lane == 0) s_row[kk] = rr;
+  }
+  __syncthreads();
+
+  const char* lt = static_cast<const char*>(a.logits) + static_cast<int64_t>(b) * a.B * a.V * esz;
+  if (wave == 0) {
+    // Lane r: the draft's probabilities under both distributions and its test.
+    const int r = lane;
+    bool rejected = false;
+    float pt = 0.f, pd = 0.f;
+    if (r < gamma) {
+      const int kr = s_row_of_step[r];
+      const bool ok = kr >= 0 && tok >= 0 && tok < a.V;
+      if (ok) {
+        const char* ld = static_cast<const char*>(a.draft_logits) +
+                         (static_cast<int64_t>(b) * a.L + r) * a.V * esz;
+        const float xt = load_elem<BF16>(lt + static_cast<int64_t>(kr) * a.V * esz, tok);
+        const float xd = load_elem<BF16>(ld, tok);
+        pt = __builtin_amdgcn_exp2f((xt - s_row[kr].mx) * a.cl) / s_row[kr].sm;
+        pd = __builtin_amdgcn_exp2f((xd - s_row[a.B + r].mx) * a.cl) / s_row[a.B + r].sm;
+      }
+      rejected = !(ok && u * pd < pt);
+    }
+    if (r < a.L) {
+      if (a.draft_prob) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = pt;
+      if (a.p_draft) a.p_draft[static_cast<int64_t>(b) * a.L + r] = pd;
+    }
+    const unsigned long long rej = __ballot(rejected);
+    const int acc = rej ? __ffsll(static_cast<long long>(rej)) - 1 : gamma;
+    if (lane == 0) {
+      a.accept_len[b] = acc;
+      s_acc = acc;
+    }
+  }
+  __syncthreads();
+  const int acc = s_acc;
+  const int kr = acc < gamma ? s_row_of_step[acc] : -1;
+  if (kr < 0) {                                // every draft accepted: no draw
+    if (tid == 0) a.correction[b] = -1;
+    return;
+  }
+
+  // The residual draw at the verification row of draft acc + 1.
+  const char* trow = lt + static_cast<int64_t>(kr) * a.V * esz;
+  const char* drow = static_cast<const char*>(a.draft_logits) +
+                     (static_cast<int64_t>(b) * a.L + acc) * a.V * esz;
+  const float mt = s_row[kr].mx, ct = 1.f / s_row[kr].sm;
+  const float md = s_row[a.B + acc].mx, cd = 1.f / s_row[a.B + acc].sm;
+  const float cl = a.cl;
+  // Weights of the VEC entries of vector v: residual (sel 0) or p_theta (sel 1).
+  auto weights = [&](int64_t v, float (&q)[VEC], float (&t)[VEC]) __attribute__((always_inline)) {
+#pragma clang fp contract(off)
+    float xt[VEC], xd[VEC];
+    load_vec<BF16, VEC>(trow, v, xt);
+    load_vec<BF16, VEC>(drow, v, xd);
+    // Both probabilities are rounded before the difference (contraction is
+    // off here: no fused multiply-subtract), so equal distributions leave an
+    // exactly empty residual, and the sums add the same rounded weights.
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      t[e] = __builtin_amdgcn_exp2f((xt[e] - mt) * cl) * ct;
+      q[e] = fmaxf(t[e] - __builtin_amdgcn_exp2f((xd[e] - md) * cl) * cd, 0.f);
+    }
+  };
+  const int64_t seg = (a.nvec + NWV - 1) / NWV;
+  const int64_t vbeg = wave * seg, vend = min(a.nvec, vbeg + seg);
+  float sq = 0.f, st = 0.f;
+  int lq = -1, lt_ = -1;
+  for (int64_t v = vbeg + lane; v < vend; v += 64) {
+    float q[VEC], t[VEC];
+    weights(v, q, t);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      sq += q[e];
+      st += t[e];
+      if (q[e] > 0.f) lq = static_cast<int>(v * VEC + e);
+      if (t[e] > 0.f) lt_ = static_cast<int>(v * VEC + e);
+    }
+  }
+#pragma unroll
+  for (int sh = 32; sh >= 1; sh >>= 1) {
+    sq += __shfl_xor(sq, sh);
+    st += __shfl_xor(st, sh);
+    lq = max(lq, __shfl_xor(lq, sh));
+    lt_ = max(lt_, __shfl_xor(lt_, sh));
+  }
+  if (lane == 0) {
+    s_tot[0][wave] = sq;
+    s_tot[1][wave] = st;
+    s_last[0][wave] = lq;
+    s_last[1][wave] = lt_;
+  }
+  __syncthreads();
+  float zq = 0.f, zt = 0.f;
+#pragma unroll
+  for (int i = 0; i < NWV; ++i) {
+    zq += s_tot[0][i];
+    zt += s_tot[1][i];
+  }
+  const int sel = zq > 0.f ? 0 : 1;
+  const float target = urow[a.L] * (sel ? zt : zq);
+  int W = -1, last = -1;
+  float base = 0.f;
+#pragma unroll
+  for (int i = 0; i < NWV; ++i) {
+    if (W < 0 && base + s_tot[sel][i] > target) W = i;
+    if (W < 0) base += s_tot[sel][i];
+    last = max(last, s_last[sel][i]);
+  }
+  if (W < 0) {                                 // the target rounded onto the total
+    if (tid == 0) a.correction[b] = last;
+    return;
+  }
+  if (wave != W) return;
+  float run = base;
+  for (int64_t v0 = W * seg; v0 < vend; v0 += 64) {
+    const int64_t v = v0 + lane;
+    float q[VEC], t[VEC];
+    float ls = 0.f;
+    if (v < vend) {
+      weights(v, q, t);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) ls += sel ? t[e] : q[e];
+    }
+    float incl = ls;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const float y = __shfl_up(incl, d);
+      if (lane >= d) incl += y;
+    }
+    const float total = __shfl(incl, 63);
+    if (run + total > target) {
+      const unsigned long long hit = __ballot(run + incl > target);
+      const int L0 = __ffsll(static_cast<long long>(hit)) - 1;
+      if (lane == L0) {
+        float rr = run + incl - ls;
+        int x = -1, xl = static_cast<int>(v * VEC);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+          const float wgt = sel ? t[e] : q[e];
+          if (wgt > 0.f) xl = static_cast<int>(v * VEC + e);
+          rr += wgt;
+          if (x < 0 && rr > target) x = static_cast<int>(v * VEC + e);
+        }
+        a.correction[b] = x >= 0 ? x : xl;
+      }
+      return;
+    }
+    run += total;
+  }
+  if (lane == 0) a.correction[b] = s_last[sel][W];   // the target rounded past this quarter
 }
 
 }  // namespace
@@ -340,16 +557,40 @@ hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const 
   const dim3 block(NT);
   const bool bf16 = d.logits_dtype == SIMSD_BF16;
   if (bf16) {
-    if (p.vec == 8) hipLaunchKernelGGL((scan_kernel<true, 8>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((scan_kernel<true, 1>), grid, block, 0, st, a);
+    if (p.vec == 8) hipLaunchKernelGGL((scan_kernel<true, 8, false>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<true, 1, false>), grid, block, 0, st, a);
   } else {
-    if (p.vec == 4) hipLaunchKernelGGL((scan_kernel<false, 4>), grid, block, 0, st, a);
-    else hipLaunchKernelGGL((scan_kernel<false, 1>), grid, block, 0, st, a);
+    if (p.vec == 4) hipLaunchKernelGGL((scan_kernel<false, 4, false>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<false, 1, false>), grid, block, 0, st, a);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (bf16) hipLaunchKernelGGL((finalize_kernel<true>), dim3(d.batch), block, 0, st, a);
   else hipLaunchKernelGGL((finalize_kernel<false>), dim3(d.batch), block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p,
+                                 const AcceptArgs& a, hipStream_t st) {
+  const dim3 grid(p.cpr, d.block_size + d.max_ref, d.batch);
+  const dim3 block(NT);
+  const bool bf16 = d.logits_dtype == SIMSD_BF16;
+  if (bf16) {
+    if (p.vec == 8) hipLaunchKernelGGL((scan_kernel<true, 8, true>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<true, 1, true>), grid, block, 0, st, a);
+  } else {
+    if (p.vec == 4) hipLaunchKernelGGL((scan_kernel<false, 4, true>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((scan_kernel<false, 1, true>), grid, block, 0, st, a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (bf16) {
+    if (p.vec == 8) hipLaunchKernelGGL((finalize_sampled_kernel<true, 8>), dim3(d.batch), block, 0, st, a);
+    else hipLaunchKernelGGL((finalize_sampled_kernel<true, 1>), dim3(d.batch), block, 0, st, a);
+  } else {
+    if (p.vec == 4) hipLaunchKernelGGL((finalize_sampled_kernel<false, 4>), dim3(d.batch), block, 0, st, a);
+    else hipLaunchKernelGGL((finalize_sampled_kernel<false, 1>), dim3(d.batch), block, 0, st, a);
+  }
   return hipGetLastError();
 }
 

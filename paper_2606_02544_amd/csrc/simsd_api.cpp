@@ -9,6 +9,8 @@
 
 using namespace simsd;
 
+static constexpr float kLog2eHost = 1.4426950408889634f;  // log2(e)
+
 static simsd_status hip_fail(hipError_t e, const char* what) {
   set_error(std::string(what) + ": " + hipGetErrorString(e));
   return SIMSD_ERR_HIP;
@@ -102,11 +104,55 @@ extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const
     a.L = desc->max_ref;
     a.V = desc->vocab;
     a.cpr = p.cpr;
+    a.rows = p.rows;
+    a.cl = kLog2eHost;
     const hipError_t e = launch_accept(*desc, p, a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept launch");
     return SIMSD_OK;
   } catch (...) {
     set_error("simsd_verify_accept: internal error");
+    return SIMSD_ERR_HIP;
+  }
+}
+
+extern "C" simsd_status simsd_verify_accept_sampled(
+    const simsd_accept_desc* desc, float temperature, const void* logits, const void* draft_logits,
+    const int32_t* draft_ids, const int32_t* step_map, const int32_t* num_ref,
+    const float* uniforms, float* p_target, float* p_draft, int32_t* accept_len,
+    int32_t* correction, void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    AcceptPlan p;
+    simsd_status st = plan_accept(desc, &p, true);
+    if (st != SIMSD_OK) return st;
+    st = check_accept_sampled_args(desc, p, temperature, logits, draft_logits, draft_ids, step_map,
+                                   num_ref, uniforms, accept_len, correction, workspace,
+                                   workspace_bytes);
+    if (st != SIMSD_OK) return st;
+    AcceptArgs a{};
+    a.logits = logits;
+    a.draft_logits = draft_logits;
+    a.draft_ids = draft_ids;
+    a.step_map = step_map;
+    a.num_ref = num_ref;
+    a.uniforms = uniforms;
+    a.draft_prob = p_target;
+    a.p_draft = p_draft;
+    a.accept_len = accept_len;
+    a.correction = correction;
+    a.part = static_cast<AcceptPartial*>(workspace);
+    a.nvec = p.nvec;
+    a.chunk_vecs = p.chunk_vecs;
+    a.B = desc->block_size;
+    a.L = desc->max_ref;
+    a.V = desc->vocab;
+    a.cpr = p.cpr;
+    a.rows = p.rows;
+    a.cl = kLog2eHost / temperature;
+    const hipError_t e = launch_accept_sampled(*desc, p, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept_sampled launch");
+    return SIMSD_OK;
+  } catch (...) {
+    set_error("simsd_verify_accept_sampled: internal error");
     return SIMSD_ERR_HIP;
   }
 }

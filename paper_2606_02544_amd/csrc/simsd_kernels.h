@@ -32,21 +32,29 @@ struct AttnArgs {
 
 struct AcceptArgs {
   const void* logits;
+  const void* draft_logits;   // sampled: [batch, L, V], same dtype as logits
   const int32_t* draft_ids;
   const int32_t* step_map;
   const int32_t* num_ref;
+  const float* uniforms;      // sampled: [batch, L + 1]
   int32_t* target_ids;
   float* confidence;
-  float* draft_prob;
+  float* draft_prob;          // greedy: target probability of each draft; sampled: p_theta(D_r)
+  float* p_draft;             // sampled: p_phi(D_r)
   int32_t* accept_len;
+  int32_t* correction;        // sampled: token drawn at the first rejection, or -1
   AcceptPartial* part;
   int64_t nvec, chunk_vecs;
   int B, L, V, cpr;
+  int rows;                   // partial rows per sequence: B, or B + L (sampled)
+  float cl;                   // log2(e) / temperature
 };
 
 hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const AttnArgs& a,
                             hipStream_t stream);
 hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const AcceptArgs& a,
                          hipStream_t stream);
+hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p,
+                                 const AcceptArgs& a, hipStream_t stream);
 
 }  // namespace simsd

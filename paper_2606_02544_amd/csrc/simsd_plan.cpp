@@ -157,7 +157,7 @@ simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, c
   return SIMSD_OK;
 }
 
-simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p) {
+simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled) {
   if (!d || !p) return fail(SIMSD_ERR_NULL_POINTER, "accept: descriptor is NULL");
   if (d->logits_dtype != SIMSD_F32 && d->logits_dtype != SIMSD_BF16)
     return fail(SIMSD_ERR_UNSUPPORTED, "accept: logits_dtype must be SIMSD_F32 or SIMSD_BF16");
@@ -170,11 +170,12 @@ simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p) {
   if (d->vocab < 1) return fail(SIMSD_ERR_BAD_SHAPE, "accept: vocab must be >= 1");
   if (d->chunks_per_row < 0) return fail(SIMSD_ERR_BAD_SHAPE, "accept: chunks_per_row < 0");
   AcceptPlan r;
+  r.rows = d->block_size + (sampled ? d->max_ref : 0);
   const int eb = elem_bytes(d->logits_dtype);
   const int w = 16 / eb;
   r.vec = (d->vocab % w == 0) ? w : 1;
   r.nvec = ceil_div(d->vocab, r.vec);
-  const int64_t rows = static_cast<int64_t>(d->batch) * d->block_size;
+  const int64_t rows = static_cast<int64_t>(d->batch) * r.rows;
   int64_t cpr = d->chunks_per_row;
   if (cpr == 0) {
     cpr = ceil_div(kAcceptTarget, rows);
@@ -211,6 +212,32 @@ simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
   return SIMSD_OK;
 }
 
+simsd_status check_accept_sampled_args(const simsd_accept_desc* d, const AcceptPlan& p,
+                                       float temperature, const void* logits,
+                                       const void* draft_logits, const int32_t* draft_ids,
+                                       const int32_t* step_map, const int32_t* num_ref,
+                                       const float* uniforms, const int32_t* accept_len,
+                                       const int32_t* correction, const void* workspace,
+                                       size_t workspace_bytes) {
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return fail(SIMSD_ERR_BAD_SHAPE, "accept_sampled: temperature must be finite and > 0");
+  if (!logits || !step_map || !num_ref || !uniforms || !accept_len || !correction)
+    return fail(SIMSD_ERR_NULL_POINTER,
+                "accept_sampled: logits, step_map, num_ref, uniforms, accept_len and correction are required");
+  if (d->max_ref > 0 && (!draft_ids || !draft_logits))
+    return fail(SIMSD_ERR_NULL_POINTER,
+                "accept_sampled: draft_ids and draft_logits required when max_ref > 0");
+  if (!aligned16(logits) || (draft_logits && !aligned16(draft_logits)))
+    return fail(SIMSD_ERR_ALIGNMENT, "accept_sampled: logits and draft_logits must be 16-byte aligned");
+  if (!workspace) return fail(SIMSD_ERR_WORKSPACE, "accept_sampled: workspace is NULL");
+  if (!aligned16(workspace))
+    return fail(SIMSD_ERR_ALIGNMENT, "accept_sampled: workspace must be 16-byte aligned");
+  if (workspace_bytes < p.workspace)
+    return fail(SIMSD_ERR_WORKSPACE,
+                "accept_sampled: workspace smaller than simsd_verify_accept_sampled_workspace_size()");
+  return SIMSD_OK;
+}
+
 }  // namespace simsd
 
 using namespace simsd;
@@ -224,6 +251,12 @@ extern "C" size_t simsd_verify_attention_workspace_size(const simsd_attn_desc* d
 extern "C" size_t simsd_verify_accept_workspace_size(const simsd_accept_desc* desc) {
   AcceptPlan p;
   if (plan_accept(desc, &p) != SIMSD_OK) return 0;
+  return p.workspace;
+}
+
+extern "C" size_t simsd_verify_accept_sampled_workspace_size(const simsd_accept_desc* desc) {
+  AcceptPlan p;
+  if (plan_accept(desc, &p, true) != SIMSD_OK) return 0;
   return p.workspace;
 }
 

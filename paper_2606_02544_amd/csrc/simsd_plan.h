@@ -40,6 +40,7 @@ struct AttnPlan {
 };
 
 struct AcceptPlan {
+  int rows = 0;           // partial rows per sequence: B (greedy) or B + L (sampled)
   int vec = 1;            // elements per vector load (16 bytes), or 1 for the scalar path
   int64_t nvec = 0;       // vectors per row
   int cpr = 0;            // chunks (work-groups) per row
@@ -66,12 +67,20 @@ simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, c
                                   const int32_t* num_ref, const void* out, const float* lse,
                                   const void* workspace, size_t workspace_bytes);
 
-simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p);
+// sampled: the stochastic entry point, whose scan also covers the L draft rows.
+simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled = false);
 simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const void* logits, const int32_t* draft_ids,
                                const int32_t* step_map, const int32_t* num_ref,
                                const int32_t* target_ids, const float* confidence,
                                const float* draft_prob, const int32_t* accept_len,
                                const void* workspace, size_t workspace_bytes);
+simsd_status check_accept_sampled_args(const simsd_accept_desc* d, const AcceptPlan& p,
+                                       float temperature, const void* logits,
+                                       const void* draft_logits, const int32_t* draft_ids,
+                                       const int32_t* step_map, const int32_t* num_ref,
+                                       const float* uniforms, const int32_t* accept_len,
+                                       const int32_t* correction, const void* workspace,
+                                       size_t workspace_bytes);
 
 }  // namespace simsd

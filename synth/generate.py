@@ -251,3 +251,54 @@ def generate(cfg: VerifyConfig, seed: Optional[int] = None, poison: bool = False
                         step_map=step_map, num_ref=num_ref, logits=logits,
                         draft_ids=draft_ids, planted=planted, seed_entropy=entropy,
                         poison=poison)
+
+
+def generate_draft_side(inp: VerifyInputs, corr: float = 0.8,
+                        threads: Optional[int] = None):
+    """Drafter-side inputs of the stochastic acceptance rule, for `inp`.
+
+    Returns (draft_logits [batch, L, V] in the config's dtype, uniforms
+    float32 [batch, L + 1] in [0, 1)).  Draft row r (r < gamma_b) is
+    corr * (the target logits of draft r's verification row) + sqrt(1 - corr^2)
+    * N(0, logit_std^2), clipped like the target rows, with the draft token's
+    own entry raised to the planting value: the drafter rated its proposal
+    highly, as it would a sampled token.  Rows past gamma_b are plain noise.
+    The uniforms are the random numbers of the rule (u_1..u_L, then the draw).
+    From child stream 10 of the sequence's SeedSequence, so the other inputs
+    are unchanged.
+    """
+    cfg = inp.cfg
+    b, B, L, V = cfg.batch, cfg.block_size, cfg.max_ref, cfg.vocab
+    s_draft = np.random.SeedSequence(inp.seed_entropy).spawn(11)[10]
+    s_rows, s_u = s_draft.spawn(2)
+    sd = np.float32(cfg.logit_std)
+    clip = np.float32(6.0 * cfg.logit_std)
+    plant_val = np.float32(6.25 * cfg.logit_std)
+    np_dtype = np.float32 if cfg.dtype == "f32" else np.uint16
+    draft_logits = np.empty((b, L, V), np_dtype)
+    row_streams = s_rows.spawn(b)
+    a, c = np.float32(corr), np.float32(np.sqrt(1.0 - corr * corr))
+
+    def as_f32(x):
+        return x if cfg.dtype == "f32" else (x.astype(np.uint32) << 16).view(np.float32)
+
+    def job(s):
+        rng = np.random.default_rng(row_streams[s])
+        gamma = int(inp.num_ref[s])
+        for r in range(L):
+            x = rng.standard_normal(V, dtype=np.float32) * sd
+            if r < gamma:
+                k = int(np.flatnonzero(inp.step_map[s] == r + 1)[0])
+                x = a * as_f32(inp.logits[s, k]) + c * x
+            np.clip(x, -clip, clip, out=x)
+            tok = int(inp.draft_ids[s, r])
+            if r < gamma and 0 <= tok < V:
+                x[tok] = plant_val
+            draft_logits[s, r] = x if cfg.dtype == "f32" else bf16_bits_from_f32(x)
+
+    nthreads = threads or min(16, os.cpu_count() or 1)
+    with cf.ThreadPoolExecutor(max_workers=nthreads) as ex:
+        list(ex.map(job, range(b)))
+    u = np.random.default_rng(s_u).random((b, L + 1)).astype(np.float32)
+    np.minimum(u, np.nextafter(np.float32(1), np.float32(0)), out=u)
+    return draft_logits, u

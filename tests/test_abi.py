@@ -178,6 +178,49 @@ def test_accept_errors():
     assert call_accept(d, ws=binding.accept_workspace_size(d) - 1) == 5
 
 
+def call_accept_sampled(desc, temperature=1.0, **over):
+    _no_gpu()
+    a = dict(logits=FAKE, draft_logits=FAKE, draft_ids=FAKE, step_map=FAKE, num_ref=FAKE,
+             uniforms=FAKE, p_target=None, p_draft=None, accept_len=FAKE, correction=FAKE,
+             workspace=FAKE, ws=1 << 30)
+    a.update(over)
+    lib = binding.lib()
+    return lib.simsd_verify_accept_sampled(
+        ctypes.byref(desc), ctypes.c_float(temperature), a["logits"], a["draft_logits"],
+        a["draft_ids"], a["step_map"], a["num_ref"], a["uniforms"], a["p_target"], a["p_draft"],
+        a["accept_len"], a["correction"], a["workspace"], a["ws"], None)
+
+
+def test_accept_sampled_errors_and_workspace():
+    good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, chunks_per_row=0,
+                logits_dtype=binding.SIMSD_BF16)
+    d = AcceptDesc(**good)
+    # the scan covers B verification rows and L draft rows per sequence
+    assert binding.accept_sampled_workspace_size(d) == 2 * 8 * d_cpr(d, 8) * 16
+    for k, v, st in [("batch", 0, 2), ("max_ref", 5, 2), ("vocab", 0, 2), ("logits_dtype", 3, 3)]:
+        assert call_accept_sampled(AcceptDesc(**dict(good, **{k: v}))) == st, k
+    for t in (0.0, -1.0, float("inf"), float("nan")):
+        assert call_accept_sampled(d, temperature=t) == 2, t
+    for k in ("logits", "draft_logits", "draft_ids", "step_map", "num_ref", "uniforms",
+              "accept_len", "correction"):
+        assert call_accept_sampled(d, **{k: None}) == 1, k
+    assert call_accept_sampled(d, draft_logits=ctypes.c_void_p(0x10008)) == 4
+    assert call_accept_sampled(d, workspace=None) == 5
+    assert call_accept_sampled(d, ws=binding.accept_sampled_workspace_size(d) - 1) == 5
+    # with L = 0 the draft inputs may be NULL
+    d0 = AcceptDesc(**dict(good, max_ref=0))
+    assert call_accept_sampled(d0, draft_logits=None, draft_ids=None, ws=0) in (0, 5)
+
+
+def d_cpr(desc, rows_per_seq):
+    """Chunks per row the plan picks: about 512 scan work-groups, at least 256
+    vectors per chunk."""
+    vec = 8 if desc.vocab % 8 == 0 else 1
+    nvec = -(-desc.vocab // vec)
+    cpr = -(-512 // (desc.batch * rows_per_seq))
+    return max(1, min(cpr, max(1, nvec // 256), nvec))
+
+
 def test_validate_step_map():
     ok = np.array([[2, 1, 0, -1, 9], [1, 2, 3, 4, 5]])
     binding.validate_step_map(ok, [2, 5], max_ref=5)
