@@ -1,9 +1,10 @@
 #!/usr/bin/env python3
 """Benchmark of the SimSD verification step on one MI355X.
 
-One step = simsd_verify_attention + simsd_verify_accept over one batch of
-seeded synthetic inputs already resident in HBM, launched back to back on one
-stream.  Prints ONE JSON line: verified tokens/s (sum over sequences of the
+One step = simsd_verify_attention + simsd_verify_accept (or, with --accept
+sampled, simsd_verify_accept_sampled: eq. 2 at temperature T with the drafter's
+logits) over one batch of seeded synthetic inputs already resident in HBM,
+launched back to back on one stream.  Prints ONE JSON line: verified tokens/s (sum over sequences of the
 drafted tokens checked per step, divided by the step time), the roofline of the
 dominant kernel (attention) measured with HIP events inside the timed region,
 and the CPU oracle's rate on a bounded sample of the same workload.
@@ -34,8 +35,9 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0
 ATTN_SOURCES = ["paper_2606_02544_amd/csrc/simsd_attention.hip"]
 
 
-def workload_numbers(inp):
-    """Algorithmic bytes and flops of one step (see the design notes)."""
+def workload_numbers(inp, sampled=False):
+    """Algorithmic bytes and flops of one step (see the design notes).  The
+    sampled rule reads the verification row and the draft row of every draft."""
     cfg = inp.cfg
     s = cfg.elem_bytes
     b, Hq, Hkv, d, n_new, B = (cfg.batch, cfg.num_q_heads, cfg.num_kv_heads, cfg.head_dim,
@@ -44,7 +46,7 @@ def workload_numbers(inp):
     kv_bytes = 2 * prefix * Hkv * d * s
     new_bytes = b * n_new * (2 * Hq * d * s + 2 * Hkv * d * s) + b * Hq * n_new * 4
     attn_bytes = kv_bytes + new_bytes
-    scanned = int(np.sum(inp.step_map >= 1))
+    scanned = 2 * int(np.sum(inp.num_ref)) if sampled else int(np.sum(inp.step_map >= 1))
     accept_bytes = scanned * cfg.vocab * s
     # every non-padded row sees prefix + (non-padded block slots) keys; QK^T and PV
     keys = 0
@@ -85,13 +87,23 @@ def recorded_traffic(workload: str):
         return None
 
 
-def cpu_baseline(inp, seconds: float, outputs=None):
+def cpu_baseline(inp, seconds: float, outputs=None, sampled=None):
     """The oracle leg.  The oracle (float64 numpy) on the same workload,
     repeated whole steps until ``seconds`` have passed, or on a subset of
     (sequence, KV head) pairs plus their sequences' accept rows when one step
-    takes longer; then, given the GPU outputs, the parity check.  Returns
-    (baseline, parity or None)."""
+    takes longer; then, given the GPU outputs, the parity check.  `sampled` =
+    (draft_logits, uniforms, T) times and checks the stochastic rule instead.
+    Returns (baseline, parity or None)."""
     import oracle
+
+    def accept_oracle(sl):
+        if sampled is None:
+            return oracle.verify_accept(inp.logits[sl], inp.draft_ids[sl], inp.step_map[sl],
+                                        inp.num_ref[sl], inp.cfg.dtype)
+        dlog, unif, T = sampled
+        return oracle.verify_accept_sampled(inp.logits[sl], dlog[sl], inp.draft_ids[sl],
+                                            inp.step_map[sl], inp.num_ref[sl],
+                                            unif[sl].astype(np.float64), T, inp.cfg.dtype)
 
     def parity_check(inp, outputs):
         """The GPU outputs of the last timed step against the oracle: attention on
@@ -112,9 +124,17 @@ def cpu_baseline(inp, seconds: float, outputs=None):
             tol = 2e-2 * ref if dt == "bf16" else np.full_like(ref, 1e-5)
             ok &= bool(np.all(err <= tol))
             ok &= bool(np.all(np.abs(l_[s_, sl] - rl[s_, sl]) <= 1e-4 * np.maximum(1, np.abs(rl[s_, sl]))))
-        rt, _, _, ra = oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, dt)
-        ok &= bool(np.array_equal(outputs["tid"].cpu().numpy(), rt))
-        ok &= bool(np.array_equal(outputs["alen"].cpu().numpy(), ra))
+        every = slice(None)
+        if sampled is None:
+            rt, _, _, ra = accept_oracle(every)
+            ok &= bool(np.array_equal(outputs["tid"].cpu().numpy(), rt))
+            ok &= bool(np.array_equal(outputs["alen"].cpu().numpy(), ra))
+        else:
+            # float32 probabilities against float64: a uniform within rounding
+            # of its threshold may fall either way (the tests move them apart)
+            _, _, ra, rc = accept_oracle(every)
+            ok &= bool(np.array_equal(outputs["alen"].cpu().numpy(), ra))
+            ok &= bool(np.array_equal(outputs["corr"].cpu().numpy(), rc))
         return {"checked": f"attention pairs {pairs}, accept all rows", "ok": ok}
 
     from threadpoolctl import threadpool_info
@@ -134,16 +154,14 @@ def cpu_baseline(inp, seconds: float, outputs=None):
             if time.perf_counter() - t0 >= seconds:
                 break
         else:
-            oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref, cfg.dtype)
+            accept_oracle(slice(None))
             steps += 1
     dt = time.perf_counter() - t0
     if steps == 0:
         # Partial step: charge the accept scan of the sampled sequences too.
         seqs = sorted({s for s, _ in pairs[:done_pairs]})
         t1 = time.perf_counter()
-        sl = np.array(seqs)
-        oracle.verify_accept(inp.logits[sl], inp.draft_ids[sl], inp.step_map[sl],
-                             inp.num_ref[sl], cfg.dtype)
+        accept_oracle(np.array(seqs))
         dt += time.perf_counter() - t1
         sample = f"{done_pairs} of {len(pairs)} (sequence, KV head) pairs + accept of {len(seqs)} sequences"
     else:
@@ -169,6 +187,9 @@ def main():
     ap.add_argument("--rotate-mb", type=float, default=640.0,
                     help="cycle input copies until this many MB are touched per cycle")
     ap.add_argument("--kv-chunk", type=int, default=0)
+    ap.add_argument("--accept", choices=["greedy", "sampled"], default="greedy",
+                    help="acceptance rule: greedy (eq. 2 at T = 0) or sampled (eq. 2 at --temperature)")
+    ap.add_argument("--temperature", type=float, default=1.0)
     ap.add_argument("--no-graph", action="store_true",
                     help="launch every kernel from Python instead of replaying HIP graphs")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
@@ -192,14 +213,16 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "launches": 5}))
         return
     from paper_2606_02544_amd import binding
-    from synth import CONFIGS, generate
+    from synth import CONFIGS, generate, generate_draft_side
 
     cfg = CONFIGS[args.config]
     torch.cuda.init()
     dev = torch.device("cuda:0")
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
     inp = generate(cfg)
-    wl = workload_numbers(inp)
+    sampled = args.accept == "sampled"
+    dlog_np, unif_np = generate_draft_side(inp) if sampled else (None, None)
+    wl = workload_numbers(inp, sampled)
     step_bytes = wl["attn_bytes"] + wl["accept_bytes"]
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / step_bytes))
     copies = min(copies, max(1, int(40e9 // step_bytes)))
@@ -218,6 +241,9 @@ def main():
                 prefix_lens=to_dev(inp.prefix_lens, "i32"), step_map=to_dev(inp.step_map, "i32"),
                 num_ref=to_dev(inp.num_ref, "i32"), logits=to_dev(inp.logits, dt),
                 draft_ids=to_dev(inp.draft_ids, "i32"))
+    if sampled:
+        base["draft_logits"] = to_dev(dlog_np, dt)
+        base["uniforms"] = torch.from_numpy(unif_np).to(dev)
     sets = [base] + [{k: (None if v is None else v.clone()) for k, v in base.items()}
                      for _ in range(copies - 1)]
 
@@ -228,6 +254,8 @@ def main():
     conf = torch.empty((b, B), dtype=torch.float32, device=dev)
     dprob = torch.empty((b, L), dtype=torch.float32, device=dev)
     alen = torch.empty((b,), dtype=torch.int32, device=dev)
+    pdraft = torch.empty((b, L), dtype=torch.float32, device=dev)
+    corr = torch.empty((b,), dtype=torch.int32, device=dev)
     adesc = binding.attention_desc(
         base["q"], base["k_cache"], num_kv_heads=cfg.num_kv_heads, block_size=B, max_ref=L,
         max_prefix_len=cfg.max_prefix, page_size=cfg.page_size,
@@ -235,7 +263,8 @@ def main():
         kv_chunk=args.kv_chunk)
     cdesc = binding.accept_desc(base["logits"], L)
     aws_n = binding.attention_workspace_size(adesc)
-    cws_n = binding.accept_workspace_size(cdesc)
+    cws_n = (binding.accept_sampled_workspace_size(cdesc) if sampled
+             else binding.accept_workspace_size(cdesc))
     aws = torch.zeros(max(aws_n, 16), dtype=torch.uint8, device=dev)
     cws = torch.zeros(max(cws_n, 16), dtype=torch.uint8, device=dev)
 
@@ -252,14 +281,21 @@ def main():
                       ptr(s["k_cache"]), ptr(s["v_cache"]), ptr(s["block_table"]),
                       ptr(s["prefix_lens"]), ptr(s["step_map"]), ptr(s["num_ref"]), ptr(out),
                       ptr(lse), ptr(aws), aws_n, sp)
-            c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]),
-                      ptr(s["step_map"]), ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob),
-                      ptr(alen), ptr(cws), cws_n, sp)
+            if sampled:
+                c_args = (ctypes.byref(cdesc), ctypes.c_float(args.temperature), ptr(s["logits"]),
+                          ptr(s["draft_logits"]), ptr(s["draft_ids"]), ptr(s["step_map"]),
+                          ptr(s["num_ref"]), ptr(s["uniforms"]), ptr(dprob), ptr(pdraft),
+                          ptr(alen), ptr(corr), ptr(cws), cws_n, sp)
+            else:
+                c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]),
+                          ptr(s["step_map"]), ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob),
+                          ptr(alen), ptr(cws), cws_n, sp)
             out_calls.append((a_args, c_args))
         return out_calls
 
     calls = build_calls(torch.cuda.current_stream())
-    f_attn, f_acc = lib.simsd_verify_attention, lib.simsd_verify_accept
+    f_attn = lib.simsd_verify_attention
+    f_acc = lib.simsd_verify_accept_sampled if sampled else lib.simsd_verify_accept
 
     def launch_step(i, what=("attn", "acc")):
         a_args, c_args = calls[i % len(calls)]
@@ -367,6 +403,7 @@ def main():
             "input_copies": copies,
             "hip_graph": use_graph,
             "kv_chunk": args.kv_chunk,
+            "accept_rule": f"sampled, temperature {args.temperature}" if sampled else "greedy",
         },
         "roofline": {
             "bound": "hbm",
@@ -381,8 +418,10 @@ def main():
         # The oracle leg: its rate on the host, and (unless --no-check) the last
         # timed step's outputs checked against it on sampled pairs.
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
-        outputs = None if args.no_check else dict(out=out, lse=lse, tid=tid, alen=alen)
-        line["cpu_baseline"], line["parity"] = cpu_baseline(inp, args.cpu_seconds, outputs)
+        outputs = None if args.no_check else dict(out=out, lse=lse, tid=tid, alen=alen, corr=corr)
+        line["cpu_baseline"], line["parity"] = cpu_baseline(
+            inp, args.cpu_seconds, outputs,
+            sampled=(dlog_np, unif_np, args.temperature) if sampled else None)
     print(json.dumps(line), flush=True)
 
 

@@ -183,18 +183,18 @@ __global__ void __launch_bounds__(NT) scan_kernel(AcceptArgs a) {
 // Partials a wave keeps in registers when it loads all its rows at once.
 constexpr int kFinalRegs = 16;
 
-// Loads the chunk partials of this wave's rows (wave, wave + NWV, ...), PPL
-// per lane per row, all before the first wait; returns them in registers.
+// Loads the chunk partials of this wave's rows (wave, wave + NWV, ... < nr),
+// PPL per lane per row, all before the first wait; returns them in registers.
 template <int PPL>
-__device__ inline void load_rows(const AcceptArgs& a, const AcceptPartial* pb, int wave, int lane,
-                                 AcceptPartial (&buf)[kFinalRegs]) {
+__device__ inline void load_rows(const AcceptArgs& a, const AcceptPartial* pb, int nr, int wave,
+                                 int lane, AcceptPartial (&buf)[kFinalRegs]) {
   constexpr int NWV = NT / 64;
   // Indices are clamped so that every load is unconditional and in bounds
   // (a guarded load would make the compiler wait on it right away); the merge
   // ignores the duplicates.
 #pragma unroll
   for (int i = 0; i < kFinalRegs; ++i) {
-    const int kk = min(wave + NWV * (i / PPL), a.B - 1), cc = min(lane + 64 * (i % PPL), a.cpr - 1);
+    const int kk = min(wave + NWV * (i / PPL), nr - 1), cc = min(lane + 64 * (i % PPL), a.cpr - 1);
     buf[i] = pb[static_cast<int64_t>(kk) * a.cpr + cc];
   }
 }
@@ -202,19 +202,19 @@ __device__ inline void load_rows(const AcceptArgs& a, const AcceptPartial* pb, i
 // cpr <= 64: the wave's rows are packed 64 / P2 to a register (P2 = cpr
 // rounded up to a power of two, lg = log2 P2), so one log2(P2)-step
 // reduction merges them all.
-__device__ inline void load_packed(const AcceptArgs& a, const AcceptPartial* pb, int wave, int lane,
-                                   int lg, AcceptPartial (&buf)[kFinalRegs]) {
+__device__ inline void load_packed(const AcceptArgs& a, const AcceptPartial* pb, int nr, int wave,
+                                   int lane, int lg, AcceptPartial (&buf)[kFinalRegs]) {
   constexpr int NWV = NT / 64;
   const int R = 64 >> lg;
 #pragma unroll
   for (int p = 0; p < kFinalRegs; ++p) {
-    const int kk = min(wave + NWV * (p * R + (lane >> lg)), a.B - 1);
+    const int kk = min(wave + NWV * (p * R + (lane >> lg)), nr - 1);
     const int cc = min(lane & ((1 << lg) - 1), a.cpr - 1);
     buf[p] = pb[static_cast<int64_t>(kk) * a.cpr + cc];
   }
 }
 
-__device__ inline void merge_packed(const AcceptArgs& a, int wave, int lane, int lg, int rpw,
+__device__ inline void merge_packed(const AcceptArgs& a, int nr, int wave, int lane, int lg, int rpw,
                                     const AcceptPartial (&buf)[kFinalRegs], Best* s_row) {
   constexpr int NWV = NT / 64;
   const int R = 64 >> lg;
@@ -224,7 +224,7 @@ __device__ inline void merge_packed(const AcceptArgs& a, int wave, int lane, int
     const int kk = wave + NWV * (p * R + (lane >> lg));
     const int cc = lane & ((1 << lg) - 1);
     Best r = {kNegInf, kNoIndex, 0.f};
-    if (cc < a.cpr && kk < a.B) r = Best{buf[p].mx, buf[p].ix, buf[p].sm};
+    if (cc < a.cpr && kk < nr) r = Best{buf[p].mx, buf[p].ix, buf[p].sm};
     for (int sh = (1 << lg) >> 1; sh >= 1; sh >>= 1) {
       Best o;
       o.mx = __shfl_xor(r.mx, sh);
@@ -232,18 +232,18 @@ __device__ inline void merge_packed(const AcceptArgs& a, int wave, int lane, int
       o.sm = __shfl_xor(r.sm, sh);
       r = combine(r, o, a.cl);
     }
-    if (cc == 0 && kk < a.B) s_row[kk] = r;
+    if (cc == 0 && kk < nr) s_row[kk] = r;
   }
 }
 
 template <int PPL>
-__device__ inline void merge_rows(const AcceptArgs& a, int wave, int lane,
+__device__ inline void merge_rows(const AcceptArgs& a, int nr, int wave, int lane,
                                   const AcceptPartial (&buf)[kFinalRegs], Best* s_row) {
   constexpr int NWV = NT / 64;
 #pragma unroll
   for (int j = 0; j < kFinalRegs / PPL; ++j) {
     const int kk = wave + NWV * j;
-    if (kk >= a.B) break;
+    if (kk >= nr) break;
     Best r = {kNegInf, kNoIndex, 0.f};
 #pragma unroll
     for (int q = 0; q < PPL; ++q) {
@@ -287,9 +287,9 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
                  : ppl <= 4 && 4 * rpw <= kFinalRegs ? 4 : 0;
   const int lg = 32 - __clz(max(a.cpr, 1) - 1);   // ceil(log2(cpr)), <= 6 in mode 1
   AcceptPartial buf[kFinalRegs];
-  if (mode == 1) load_packed(a, pb, wave, lane, lg, buf);
-  else if (mode == 2) load_rows<2>(a, pb, wave, lane, buf);
-  else if (mode == 4) load_rows<4>(a, pb, wave, lane, buf);
+  if (mode == 1) load_packed(a, pb, a.B, wave, lane, lg, buf);
+  else if (mode == 2) load_rows<2>(a, pb, a.B, wave, lane, buf);
+  else if (mode == 4) load_rows<4>(a, pb, a.B, wave, lane, buf);
   if (tid < a.B) s_step[tid] = step_t;
   if (tid < kMaxNew) s_row_of_step[tid] = -1;
   const int gamma = min(max(nref, 0), a.L);
@@ -307,9 +307,9 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
       x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
   }
 
-  if (mode == 1) merge_packed(a, wave, lane, lg, rpw, buf, s_row);
-  else if (mode == 2) merge_rows<2>(a, wave, lane, buf, s_row);
-  else if (mode == 4) merge_rows<4>(a, wave, lane, buf, s_row);
+  if (mode == 1) merge_packed(a, a.B, wave, lane, lg, rpw, buf, s_row);
+  else if (mode == 2) merge_rows<2>(a, a.B, wave, lane, buf, s_row);
+  else if (mode == 4) merge_rows<4>(a, a.B, wave, lane, buf, s_row);
   else {
     for (int kk = wave; kk < a.B; kk += NWV) {
       Best rr = {kNegInf, kNoIndex, 0.f};
@@ -351,26 +351,50 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
 // prefix ends at the first rejection, where the token is drawn from the
 // residual max(0, p_theta - p_phi) (or p_theta when that is empty everywhere)
 // by inverse CDF in vocabulary order with the uniform w = uniforms[b, L].
-// One work-group per sequence.  The draw reads the two rows twice: once for
-// per-wave totals (each wave owns a contiguous quarter of the vocabulary,
-// read in coalesced stripes), then, in the wave whose quarter holds the
-// target w * Z, stripe by stripe with a wave prefix sum until the running sum
-// passes it.
+// After the scan, accept_sampled_kernel runs draw_chunks work-groups per
+// sequence: each merges the chunk partials of the rows it needs and takes the
+// acceptance decision (cheap, so every group repeats it), group 0 writes the
+// per-draft outputs, and every group sums the residual and p_theta over its
+// vocabulary chunk.  draw_pick_kernel (one group per sequence) then finds the
+// chunk where the running sum passes w * Z and the entry inside it.
+
+// Weights of the VEC entries of vector v of the draw rows: the residual in q,
+// p_theta in t.  Both probabilities are rounded before the difference
+// (contraction off: no fused multiply-subtract), so equal distributions leave
+// an exactly empty residual and every pass adds the same rounded weights.
+template <int VEC>
+__device__ inline void draw_weights(const float (&xt)[VEC], const float (&xd)[VEC], const DrawRow& r,
+                                    float cl, float (&q)[VEC], float (&t)[VEC]) {
+#pragma clang fp contract(off)
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    t[e] = __builtin_amdgcn_exp2f((xt[e] - r.mt) * cl) * r.ct;
+    q[e] = fmaxf(t[e] - __builtin_amdgcn_exp2f((xd[e] - r.md) * cl) * r.cd, 0.f);
+  }
+}
+
+template <bool BF16>
+__device__ inline void draw_rows(const AcceptArgs& a, int b, const DrawRow& r, const char*& trow,
+                                 const char*& drow) {
+  const int esz = BF16 ? 2 : 4;
+  trow = static_cast<const char*>(a.logits) + (static_cast<int64_t>(b) * a.B + r.kr) * a.V * esz;
+  drow = static_cast<const char*>(a.draft_logits) + (static_cast<int64_t>(b) * a.L + r.acc) * a.V * esz;
+}
+
 template <bool BF16, int VEC>
-__global__ void __launch_bounds__(NT) finalize_sampled_kernel(AcceptArgs a) {
+__global__ void __launch_bounds__(NT) accept_sampled_kernel(AcceptArgs a) {
   constexpr int NWV = NT / 64;
   __shared__ Best s_row[2 * kMaxNew];        // [0, B): verification rows; B + r: draft row r
   __shared__ int s_step[kMaxNew];
   __shared__ int s_row_of_step[kMaxNew];
-  __shared__ float s_tot[2][NWV];            // per-wave sums: residual, p_theta
-  __shared__ int s_last[2][NWV];             // per-wave last index of positive weight
   __shared__ int s_acc;
-  const int b = blockIdx.x;
+  __shared__ float s_sum[2][NWV];
+  __shared__ int s_last[2][NWV];
+  const int c = blockIdx.x, b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int esz = BF16 ? 2 : 4;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(b) * a.B;
   const AcceptPartial* pb = a.part + static_cast<int64_t>(b) * a.rows * a.cpr;
-  const float* urow = a.uniforms + static_cast<int64_t>(b) * (a.L + 1);
 
   // First round of loads, none waiting on another (see finalize_kernel).
   int lane_zero;
@@ -379,24 +403,38 @@ __global__ void __launch_bounds__(NT) finalize_sampled_kernel(AcceptArgs a) {
   const int step_t = step_row[min(tid, a.B - 1)];
   int tok = -1;
   if (a.L > 0) tok = a.draft_ids[static_cast<int64_t>(b) * a.L + min(lane, a.L - 1)];
-  const float u = urow[min(lane, a.L)];
+  const float u = a.uniforms[static_cast<int64_t>(b) * (a.L + 1) + min(lane, a.L)];
+  // The chunk partials of all B + L rows, loaded with the first round as in
+  // finalize_kernel (rows this step did not scan hold stale values, unused).
+  const int nr = a.B + a.L;
+  const int rpw = (nr + NWV - 1) / NWV;
+  const int ppl = (a.cpr + 63) / 64;
+  const int mode = ppl == 1 && rpw <= kFinalRegs ? 1 : ppl == 2 && 2 * rpw <= kFinalRegs ? 2
+                 : ppl <= 4 && 4 * rpw <= kFinalRegs ? 4 : 0;
+  const int lg = 32 - __clz(max(a.cpr, 1) - 1);
+  AcceptPartial buf[kFinalRegs];
+  if (mode == 1) load_packed(a, pb, nr, wave, lane, lg, buf);
+  else if (mode == 2) load_rows<2>(a, pb, nr, wave, lane, buf);
+  else if (mode == 4) load_rows<4>(a, pb, nr, wave, lane, buf);
   const int gamma = min(max(nref, 0), a.L);
   if (tid < a.B) s_step[tid] = step_t;
   if (tid < kMaxNew) s_row_of_step[tid] = -1;
   __syncthreads();
   if (tid < a.B && step_t >= 1 && step_t <= gamma) s_row_of_step[step_t - 1] = tid;
-
-  // Merge the chunks of the rows the step reads (verification rows of steps
-  // 1..gamma, draft rows 0..gamma-1).
-  for (int kk = wave; kk < a.B + gamma; kk += NWV) {
-    if (kk < a.B && !(s_step[kk] >= 1 && s_step[kk] <= gamma)) continue;
-    Best rr = {kNegInf, kNoIndex, 0.f};
-    for (int cc = lane; cc < a.cpr; cc += 64) {
-      const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
-      rr = combine(rr, Best{pr.mx, pr.ix, pr.sm}, a.cl);
+  if (mode == 1) merge_packed(a, nr, wave, lane, lg, rpw, buf, s_row);
+  else if (mode == 2) merge_rows<2>(a, nr, wave, lane, buf, s_row);
+  else if (mode == 4) merge_rows<4>(a, nr, wave, lane, buf, s_row);
+  else {
+    for (int kk = wave; kk < a.B + gamma; kk += NWV) {
+      if (kk < a.B && !(s_step[kk] >= 1 && s_step[kk] <= gamma)) continue;
+      Best rr = {kNegInf, kNoIndex, 0.f};
+      for (int cc = lane; cc < a.cpr; cc += 64) {
+        const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
+        rr = combine(rr, Best{pr.mx, pr.ix, pr.sm}, a.cl);
+      }
+      rr = wave_reduce(rr, a.cl);
+      if (lane == 0) s_row[kk] = rr;
     }
-    rr = wave_reduce(rr, a.cl);
-    if (lane == 0) s_row[kk] = rr;
   }
   __syncthreads();
 
@@ -419,54 +457,46 @@ __global__ void __launch_bounds__(NT) finalize_sampled_kernel(AcceptArgs a) {
       }
       rejected = !(ok && u * pd < pt);
     }
-    if (r < a.L) {
-      if (a.draft_prob) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = pt;
-      if (a.p_draft) a.p_draft[static_cast<int64_t>(b) * a.L + r] = pd;
-    }
     const unsigned long long rej = __ballot(rejected);
     const int acc = rej ? __ffsll(static_cast<long long>(rej)) - 1 : gamma;
-    if (lane == 0) {
-      a.accept_len[b] = acc;
-      s_acc = acc;
+    if (c == 0) {
+      if (r < a.L) {
+        if (a.draft_prob) a.draft_prob[static_cast<int64_t>(b) * a.L + r] = pt;
+        if (a.p_draft) a.p_draft[static_cast<int64_t>(b) * a.L + r] = pd;
+      }
+      if (lane == 0) a.accept_len[b] = acc;
     }
+    if (lane == 0) s_acc = acc;
   }
   __syncthreads();
   const int acc = s_acc;
-  const int kr = acc < gamma ? s_row_of_step[acc] : -1;
-  if (kr < 0) {                                // every draft accepted: no draw
-    if (tid == 0) a.correction[b] = -1;
+  DrawRow dr;
+  dr.acc = acc;
+  dr.kr = acc < gamma ? s_row_of_step[acc] : -1;
+  if (dr.kr < 0) {                             // every draft accepted: no draw
+    if (c == 0 && tid == 0) {
+      a.correction[b] = -1;
+      a.draw_row[b] = dr;
+    }
     return;
   }
+  dr.mt = s_row[dr.kr].mx;
+  dr.ct = 1.f / s_row[dr.kr].sm;
+  dr.md = s_row[a.B + acc].mx;
+  dr.cd = 1.f / s_row[a.B + acc].sm;
+  if (c == 0 && tid == 0) a.draw_row[b] = dr;
 
-  // The residual draw at the verification row of draft acc + 1.
-  const char* trow = lt + static_cast<int64_t>(kr) * a.V * esz;
-  const char* drow = static_cast<const char*>(a.draft_logits) +
-                     (static_cast<int64_t>(b) * a.L + acc) * a.V * esz;
-  const float mt = s_row[kr].mx, ct = 1.f / s_row[kr].sm;
-  const float md = s_row[a.B + acc].mx, cd = 1.f / s_row[a.B + acc].sm;
-  const float cl = a.cl;
-  // Weights of the VEC entries of vector v: residual (sel 0) or p_theta (sel 1).
-  auto weights = [&](int64_t v, float (&q)[VEC], float (&t)[VEC]) __attribute__((always_inline)) {
-#pragma clang fp contract(off)
-    float xt[VEC], xd[VEC];
-    load_vec<BF16, VEC>(trow, v, xt);
-    load_vec<BF16, VEC>(drow, v, xd);
-    // Both probabilities are rounded before the difference (contraction is
-    // off here: no fused multiply-subtract), so equal distributions leave an
-    // exactly empty residual, and the sums add the same rounded weights.
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) {
-      t[e] = __builtin_amdgcn_exp2f((xt[e] - mt) * cl) * ct;
-      q[e] = fmaxf(t[e] - __builtin_amdgcn_exp2f((xd[e] - md) * cl) * cd, 0.f);
-    }
-  };
-  const int64_t seg = (a.nvec + NWV - 1) / NWV;
-  const int64_t vbeg = wave * seg, vend = min(a.nvec, vbeg + seg);
+  // This group's vocabulary chunk of the draw row: sums and last positive entries.
+  const char *trow, *drow;
+  draw_rows<BF16>(a, b, dr, trow, drow);
+  const int64_t v0 = static_cast<int64_t>(c) * a.draw_vecs, v1 = min(a.nvec, v0 + a.draw_vecs);
   float sq = 0.f, st = 0.f;
   int lq = -1, lt_ = -1;
-  for (int64_t v = vbeg + lane; v < vend; v += 64) {
-    float q[VEC], t[VEC];
-    weights(v, q, t);
+  for (int64_t v = v0 + tid; v < v1; v += NT) {
+    float xt[VEC], xd[VEC], q[VEC], t[VEC];
+    load_vec<BF16, VEC>(trow, v, xt);
+    load_vec<BF16, VEC>(drow, v, xd);
+    draw_weights<VEC>(xt, xd, dr, a.cl, q, t);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       sq += q[e];
@@ -483,70 +513,153 @@ __global__ void __launch_bounds__(NT) finalize_sampled_kernel(AcceptArgs a) {
     lt_ = max(lt_, __shfl_xor(lt_, sh));
   }
   if (lane == 0) {
-    s_tot[0][wave] = sq;
-    s_tot[1][wave] = st;
+    s_sum[0][wave] = sq;
+    s_sum[1][wave] = st;
     s_last[0][wave] = lq;
     s_last[1][wave] = lt_;
   }
   __syncthreads();
-  float zq = 0.f, zt = 0.f;
-#pragma unroll
-  for (int i = 0; i < NWV; ++i) {
-    zq += s_tot[0][i];
-    zt += s_tot[1][i];
+  if (tid == 0) {
+    DrawPartial dp = {0.f, 0.f, -1, -1};
+    for (int i = 0; i < NWV; ++i) {
+      dp.sq += s_sum[0][i];
+      dp.st += s_sum[1][i];
+      dp.lq = max(dp.lq, s_last[0][i]);
+      dp.lt = max(dp.lt, s_last[1][i]);
+    }
+    a.draw_part[static_cast<int64_t>(b) * a.draw_chunks + c] = dp;
   }
-  const int sel = zq > 0.f ? 0 : 1;
-  const float target = urow[a.L] * (sel ? zt : zq);
-  int W = -1, last = -1;
-  float base = 0.f;
+}
+
+// Inclusive prefix sums of two values over the work-group's threads (thread
+// order).
+__device__ inline float2 block_inclusive_scan2(float2 x, float2* s_wave, int lane, int wave) {
+  constexpr int NWV = NT / 64;
 #pragma unroll
-  for (int i = 0; i < NWV; ++i) {
-    if (W < 0 && base + s_tot[sel][i] > target) W = i;
-    if (W < 0) base += s_tot[sel][i];
-    last = max(last, s_last[sel][i]);
+  for (int d = 1; d < 64; d <<= 1) {
+    const float y0 = __shfl_up(x.x, d), y1 = __shfl_up(x.y, d);
+    if (lane >= d) {
+      x.x += y0;
+      x.y += y1;
+    }
   }
-  if (W < 0) {                                 // the target rounded onto the total
-    if (tid == 0) a.correction[b] = last;
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  float2 base = {0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < NWV; ++i)
+    if (i < wave) {
+      base.x += s_wave[i].x;
+      base.y += s_wave[i].y;
+    }
+  __syncthreads();
+  return float2{base.x + x.x, base.y + x.y};
+}
+
+// One work-group per sequence with a draw: the chunk where the running sum
+// passes w * Z (one prefix sum over the chunk sums), then inside that chunk
+// each thread takes a contiguous run of vectors, so one more prefix sum over
+// the threads' run sums finds the thread, which walks its run.
+template <bool BF16, int VEC>
+__global__ void __launch_bounds__(NT) draw_pick_kernel(AcceptArgs a) {
+  constexpr int RB = 4;                        // vectors of a run loaded at once
+  __shared__ float2 s_wave[NT / 64];
+  __shared__ float2 s_tot;
+  __shared__ int s_hit, s_last;
+  __shared__ float s_base;
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // The chunk partials (draw_chunks <= NT) load with the draw row.
+  const DrawPartial* pp = a.draw_part + static_cast<int64_t>(b) * a.draw_chunks;
+  DrawPartial mine = {0.f, 0.f, -1, -1};
+  if (tid < a.draw_chunks) mine = pp[tid];
+  const DrawRow dr = a.draw_row[b];
+  const float w = a.uniforms[static_cast<int64_t>(b) * (a.L + 1) + a.L];
+  if (dr.kr < 0) return;                       // no draw (correction already -1)
+
+  const float2 incl = block_inclusive_scan2(float2{mine.sq, mine.st}, s_wave, lane, wave);
+  if (tid == NT - 1) s_tot = incl;
+  if (tid == 0) {
+    s_hit = NT;
+    s_last = -1;
+  }
+  __syncthreads();
+  const int sel = s_tot.x > 0.f ? 0 : 1;       // empty residual: draw from p_theta
+  const float target = w * (sel ? s_tot.y : s_tot.x);
+  const float mi = sel ? incl.y : incl.x, my = sel ? mine.st : mine.sq;
+  const int mylast = sel ? mine.lt : mine.lq;
+  if (tid < a.draw_chunks) {
+    if (mi > target) atomicMin(&s_hit, tid);
+    atomicMax(&s_last, mylast);
+  }
+  __syncthreads();
+  const int C = s_hit;
+  if (C >= a.draw_chunks) {                    // the target rounded onto the total
+    if (tid == 0) a.correction[b] = s_last;
     return;
   }
-  if (wave != W) return;
-  float run = base;
-  for (int64_t v0 = W * seg; v0 < vend; v0 += 64) {
-    const int64_t v = v0 + lane;
-    float q[VEC], t[VEC];
-    float ls = 0.f;
-    if (v < vend) {
-      weights(v, q, t);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) ls += sel ? t[e] : q[e];
-    }
-    float incl = ls;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const float y = __shfl_up(incl, d);
-      if (lane >= d) incl += y;
-    }
-    const float total = __shfl(incl, 63);
-    if (run + total > target) {
-      const unsigned long long hit = __ballot(run + incl > target);
-      const int L0 = __ffsll(static_cast<long long>(hit)) - 1;
-      if (lane == L0) {
-        float rr = run + incl - ls;
-        int x = -1, xl = static_cast<int>(v * VEC);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const float wgt = sel ? t[e] : q[e];
-          if (wgt > 0.f) xl = static_cast<int>(v * VEC + e);
-          rr += wgt;
-          if (x < 0 && rr > target) x = static_cast<int>(v * VEC + e);
-        }
-        a.correction[b] = x >= 0 ? x : xl;
-      }
-      return;
-    }
-    run += total;
+  __syncthreads();
+  if (tid == C) {
+    s_base = mi - my;
+    s_last = mylast;
   }
-  if (lane == 0) a.correction[b] = s_last[sel][W];   // the target rounded past this quarter
+  __syncthreads();
+  const float base = s_base;
+  const int clast = s_last;
+
+  // Chunk C: thread tid owns vectors [c0, c1), a contiguous run.
+  const char *trow, *drow;
+  draw_rows<BF16>(a, b, dr, trow, drow);
+  const int64_t v0 = static_cast<int64_t>(C) * a.draw_vecs, v1 = min(a.nvec, v0 + a.draw_vecs);
+  const int64_t k = (v1 - v0 + NT - 1) / NT;
+  const int64_t c0 = min(v1, v0 + tid * k), c1 = min(v1, c0 + k);
+  float ls = 0.f;
+  for (int64_t vb = c0; vb < c1; vb += RB) {
+    float xt[RB][VEC], xd[RB][VEC];
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      if (vb + r < c1) {
+        load_vec<BF16, VEC>(trow, vb + r, xt[r]);
+        load_vec<BF16, VEC>(drow, vb + r, xd[r]);
+      }
+#pragma unroll
+    for (int r = 0; r < RB; ++r)
+      if (vb + r < c1) {
+        float q[VEC], t[VEC];
+        draw_weights<VEC>(xt[r], xd[r], dr, a.cl, q, t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) ls += sel ? t[e] : q[e];
+      }
+  }
+  const float2 in2 = block_inclusive_scan2(float2{ls, 0.f}, s_wave, lane, wave);
+  const float in = base + in2.x;
+  if (tid == 0) s_hit = NT;
+  __syncthreads();
+  if (c0 < c1 && in > target) atomicMin(&s_hit, tid);
+  __syncthreads();
+  const int T0 = s_hit;
+  if (T0 >= NT) {                              // the target rounded past this chunk
+    if (tid == 0) a.correction[b] = clast;
+    return;
+  }
+  if (tid != T0) return;
+  // Walk the run (its vectors are re-read: cache hits) in the same order.
+  float rr = in - ls;
+  int x = -1, xl = static_cast<int>(c0 * VEC);
+  for (int64_t v = c0; v < c1 && x < 0; ++v) {
+    float xt[VEC], xd[VEC], q[VEC], t[VEC];
+    load_vec<BF16, VEC>(trow, v, xt);
+    load_vec<BF16, VEC>(drow, v, xd);
+    draw_weights<VEC>(xt, xd, dr, a.cl, q, t);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const float wgt = sel ? t[e] : q[e];
+      if (wgt > 0.f) xl = static_cast<int>(v * VEC + e);
+      rr += wgt;
+      if (x < 0 && rr > target) x = static_cast<int>(v * VEC + e);
+    }
+  }
+  a.correction[b] = x >= 0 ? x : xl;
 }
 
 }  // namespace
@@ -584,12 +697,23 @@ hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const dim3 dgrid(p.draw_chunks, d.batch);
   if (bf16) {
-    if (p.vec == 8) hipLaunchKernelGGL((finalize_sampled_kernel<true, 8>), dim3(d.batch), block, 0, st, a);
-    else hipLaunchKernelGGL((finalize_sampled_kernel<true, 1>), dim3(d.batch), block, 0, st, a);
+    if (p.vec == 8) {
+      hipLaunchKernelGGL((accept_sampled_kernel<true, 8>), dgrid, block, 0, st, a);
+      hipLaunchKernelGGL((draw_pick_kernel<true, 8>), dim3(d.batch), block, 0, st, a);
+    } else {
+      hipLaunchKernelGGL((accept_sampled_kernel<true, 1>), dgrid, block, 0, st, a);
+      hipLaunchKernelGGL((draw_pick_kernel<true, 1>), dim3(d.batch), block, 0, st, a);
+    }
   } else {
-    if (p.vec == 4) hipLaunchKernelGGL((finalize_sampled_kernel<false, 4>), dim3(d.batch), block, 0, st, a);
-    else hipLaunchKernelGGL((finalize_sampled_kernel<false, 1>), dim3(d.batch), block, 0, st, a);
+    if (p.vec == 4) {
+      hipLaunchKernelGGL((accept_sampled_kernel<false, 4>), dgrid, block, 0, st, a);
+      hipLaunchKernelGGL((draw_pick_kernel<false, 4>), dim3(d.batch), block, 0, st, a);
+    } else {
+      hipLaunchKernelGGL((accept_sampled_kernel<false, 1>), dgrid, block, 0, st, a);
+      hipLaunchKernelGGL((draw_pick_kernel<false, 1>), dim3(d.batch), block, 0, st, a);
+    }
   }
   return hipGetLastError();
 }

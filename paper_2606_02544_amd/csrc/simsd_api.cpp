@@ -148,6 +148,10 @@ extern "C" simsd_status simsd_verify_accept_sampled(
     a.cpr = p.cpr;
     a.rows = p.rows;
     a.cl = kLog2eHost / temperature;
+    a.draw_chunks = p.draw_chunks;
+    a.draw_vecs = p.draw_vecs;
+    a.draw_row = reinterpret_cast<DrawRow*>(static_cast<char*>(workspace) + p.draw_row_off);
+    a.draw_part = reinterpret_cast<DrawPartial*>(static_cast<char*>(workspace) + p.draw_part_off);
     const hipError_t e = launch_accept_sampled(*desc, p, a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept_sampled launch");
     return SIMSD_OK;

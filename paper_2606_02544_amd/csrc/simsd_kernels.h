@@ -44,8 +44,10 @@ struct AcceptArgs {
   int32_t* accept_len;
   int32_t* correction;        // sampled: token drawn at the first rejection, or -1
   AcceptPartial* part;
-  int64_t nvec, chunk_vecs;
-  int B, L, V, cpr;
+  DrawRow* draw_row;          // sampled: [batch]
+  DrawPartial* draw_part;     // sampled: [batch, draw_chunks]
+  int64_t nvec, chunk_vecs, draw_vecs;
+  int B, L, V, cpr, draw_chunks;
   int rows;                   // partial rows per sequence: B, or B + L (sampled)
   float cl;                   // log2(e) / temperature
 };

@@ -187,6 +187,17 @@ simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled
   r.cpr = static_cast<int>(cpr);
   r.chunk_vecs = ceil_div(r.nvec, r.cpr);
   r.workspace = static_cast<size_t>(rows) * r.cpr * sizeof(AcceptPartial);
+  if (sampled) {
+    // About kAcceptTarget draw work-groups, each at least one vector per thread.
+    int64_t g = ceil_div(kAcceptTarget, d->batch);
+    const int64_t most = std::max<int64_t>(1, r.nvec / kAcceptThreads);
+    g = std::min<int64_t>(std::min<int64_t>(g, most), kAcceptThreads);
+    r.draw_chunks = static_cast<int>(std::max<int64_t>(g, 1));
+    r.draw_vecs = ceil_div(r.nvec, r.draw_chunks);
+    r.draw_row_off = (r.workspace + 255) / 256 * 256;
+    r.draw_part_off = r.draw_row_off + static_cast<size_t>(d->batch) * sizeof(DrawRow);
+    r.workspace = r.draw_part_off + static_cast<size_t>(d->batch) * r.draw_chunks * sizeof(DrawPartial);
+  }
   *p = r;
   return SIMSD_OK;
 }

@@ -41,6 +41,10 @@ struct AttnPlan {
 
 struct AcceptPlan {
   int rows = 0;           // partial rows per sequence: B (greedy) or B + L (sampled)
+  int draw_chunks = 0;    // sampled: vocabulary chunks of the residual draw per sequence
+  int64_t draw_vecs = 0;  // sampled: vectors per draw chunk
+  size_t draw_row_off = 0;   // sampled: workspace offsets (bytes) of the per-sequence
+  size_t draw_part_off = 0;  //   draw rows and of the draw chunk partials
   int vec = 1;            // elements per vector load (16 bytes), or 1 for the scalar path
   int64_t nvec = 0;       // vectors per row
   int cpr = 0;            // chunks (work-groups) per row
@@ -55,6 +59,21 @@ struct AcceptPartial {
   int32_t ix;
   float sm;
   int32_t pad;
+};
+
+// Sampled rule: what the draw needs of one sequence (written once the
+// acceptance is decided; acc >= gamma, kr = -1 when every draft was accepted).
+struct DrawRow {
+  int32_t acc, kr;
+  float mt, ct, md, cd;   // row maxima and reciprocal sums of the two rows
+  int32_t pad[2];
+};
+
+// Sampled rule: one vocabulary chunk of the draw row: sums of the residual
+// and of p_theta, and the last index of each with positive weight.
+struct DrawPartial {
+  float sq, st;
+  int32_t lq, lt;
 };
 
 void set_error(const std::string& msg);

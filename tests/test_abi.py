@@ -195,8 +195,15 @@ def test_accept_sampled_errors_and_workspace():
     good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, chunks_per_row=0,
                 logits_dtype=binding.SIMSD_BF16)
     d = AcceptDesc(**good)
-    # the scan covers B verification rows and L draft rows per sequence
-    assert binding.accept_sampled_workspace_size(d) == 2 * 8 * d_cpr(d, 8) * 16
+    # the scan covers B verification rows and L draft rows per sequence (16-byte
+    # partials), then 256-byte alignment, one 32-byte draw row per sequence and
+    # 16-byte draw partials per vocabulary chunk (V = 1000: one chunk)
+    rows = 2 * 8 * d_cpr(d, 8) * 16
+    assert binding.accept_sampled_workspace_size(d) == -(-rows // 256) * 256 + 2 * 32 + 2 * 1 * 16
+    big = AcceptDesc(batch=16, block_size=32, max_ref=32, vocab=151936, chunks_per_row=0,
+                     logits_dtype=binding.SIMSD_BF16)
+    # 1024 scanned rows -> 1 chunk each; 32 draw chunks per sequence (about 512 groups)
+    assert binding.accept_sampled_workspace_size(big) == 16 * 64 * 16 + 16 * 32 + 16 * 32 * 16
     for k, v, st in [("batch", 0, 2), ("max_ref", 5, 2), ("vocab", 0, 2), ("logits_dtype", 3, 3)]:
         assert call_accept_sampled(AcceptDesc(**dict(good, **{k: v}))) == st, k
     for t in (0.0, -1.0, float("inf"), float("nan")):
