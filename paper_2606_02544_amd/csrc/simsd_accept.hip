@@ -1,4 +1,4 @@
-// Vocabulary scan and greedy acceptance of SimSD on gfx950.
+// Vocabulary scan and acceptance of SimSD on gfx950.
 //
 // Eq. 2 at temperature 0 (Sec. 3.2): draft r is accepted while the target's
 // argmax at its verification slot equals it, and the longest such prefix is
@@ -11,6 +11,11 @@
 // and every chunk partial of its rows; then the drafted tokens' logits),
 // merges the chunks, computes confidence and draft probabilities and finds the
 // accepted prefix with one wave ballot.
+//
+// The stochastic form of eq. 2 (temperature T, caller-supplied uniforms) runs
+// the same scan over the verification rows and the drafter's rows, then the
+// acceptance test and the residual draw of the first rejection (see the
+// section further down).
 #include "simsd_kernels.h"
 
 namespace simsd {
