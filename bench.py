@@ -56,7 +56,7 @@ def workload_numbers(inp, sampled=False):
         keys += rows * (int(inp.prefix_lens[q]) + nonpad)
     attn_flops = 4 * keys * Hq * d
     return dict(attn_bytes=attn_bytes, accept_bytes=accept_bytes, attn_flops=attn_flops,
-                verified=int(np.sum(inp.num_ref)))
+                verified=int(np.sum(inp.num_ref)), scanned_rows=int(np.sum(inp.step_map >= 1)))
 
 
 def source_digest(paths):
@@ -190,6 +190,11 @@ def main():
     ap.add_argument("--accept", choices=["greedy", "sampled"], default="greedy",
                     help="acceptance rule: greedy (eq. 2 at T = 0) or sampled (eq. 2 at --temperature)")
     ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--gamma", type=int, default=None,
+                    help="drafts per step (reference slots L = gamma <= B; default: the workload's); "
+                         "0 = the plain block step once fewer than gamma positions remain")
+    ap.add_argument("--committed", type=int, default=0,
+                    help="block slots already committed by earlier steps of the block")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch every kernel from Python instead of replaying HIP graphs")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
@@ -216,6 +221,13 @@ def main():
     from synth import CONFIGS, generate, generate_draft_side
 
     cfg = CONFIGS[args.config]
+    custom = args.gamma is not None or args.committed
+    if custom:
+        import dataclasses
+        g = cfg.max_ref if args.gamma is None else args.gamma
+        if not 0 <= g <= cfg.block_size or not 0 <= args.committed <= cfg.block_size - g:
+            sys.exit(f"need 0 <= gamma <= {cfg.block_size} and 0 <= committed <= B - gamma")
+        cfg = dataclasses.replace(cfg, max_ref=g, committed=args.committed)
     torch.cuda.init()
     dev = torch.device("cuda:0")
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
@@ -374,7 +386,7 @@ def main():
 
     value = wl["verified"] * K / elapsed
     attn_gbs = wl["attn_bytes"] / (attn_ms * 1e-3) / 1e9
-    traffic = recorded_traffic(cfg.name)
+    traffic = None if custom else recorded_traffic(cfg.name)
     line = {
         "metric": METRIC,
         "value": value,
@@ -392,6 +404,7 @@ def main():
             "workload": f"{cfg.name}: batch {b}, {cfg.num_q_heads}/{cfg.num_kv_heads} heads, "
                         f"head_dim {cfg.head_dim}, prefix {cfg.prefix}, block {B}, "
                         f"{L} reference slots, vocab {cfg.vocab}"
+                        + (f", gamma {L}, {cfg.committed} committed" if custom else "")
                         + (f", paged {cfg.page_size}" if cfg.page_size else ""),
             "step_hbm_bytes": step_bytes,
             "step_hbm_gbs": step_bytes / (elapsed / K) / 1e9,
@@ -399,6 +412,7 @@ def main():
             "attention_us": attn_ms * 1e3,
             "accept_us": acc_ms * 1e3,
             "accept_gbs": wl["accept_bytes"] / (acc_ms * 1e-3) / 1e9,
+            "scanned_rows_per_s": wl["scanned_rows"] * K / elapsed,
             "attention_mfma_frac": wl["attn_flops"] / (attn_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
             "input_copies": copies,
             "hip_graph": use_graph,

@@ -29,9 +29,12 @@ class VerifyConfig:
                 are laid out in a seeded random order.
     plant       probability that a drafted token is planted as the unique argmax
                 of its verification row, or a (lo, hi) range drawn per sequence.
-    step_mode   "full": every block slot drafted, step map a random permutation of
-                1..B (the paper's setting, gamma = B).  "mixed": per-sequence gamma,
+    step_mode   "full": gamma = L drafted slots in a random order (the paper's
+                setting is L = B), `committed` slots decoded by earlier steps of
+                the block, the rest not drafted.  "mixed": per-sequence gamma,
                 committed, undrafted and padding slots (test cases).
+    committed   "full" mode: block slots already committed (a later verification
+                step inside the block), at most B - L.
     """
 
     cid: int
@@ -51,6 +54,7 @@ class VerifyConfig:
     logit_std: float = 2.0     # N(0, 4): variance 4
     step_mode: str = "full"
     capacity: int = 0          # contiguous cache rows per sequence; 0 = max prefix
+    committed: int = 0
 
     @property
     def n_new(self) -> int:

@@ -108,7 +108,8 @@ def _step_maps(rng, cfg: VerifyConfig):
     for s in range(b):
         if cfg.step_mode == "full":
             gamma = min(L, B)
-            n_pad = n_com = 0
+            n_pad = 0
+            n_com = min(cfg.committed, B - gamma)
         elif cfg.step_mode == "mixed":
             n_pad = int(rng.integers(0, B // 4 + 1))
             n_com = int(rng.integers(0, (B - n_pad) // 2 + 1))

@@ -41,6 +41,21 @@ def test_config_full(cid):
     _full_parity(inp)
 
 
+@pytest.mark.parametrize("gamma,committed", [(8, 0), (3, 0), (3, 2), (0, 0), (0, 5)])
+def test_steps_inside_a_block(gamma, committed):
+    """A verification step with gamma < B drafts (the paper's gamma ablation,
+    Table 3, at B = 8), later steps of the block with committed slots, and the
+    plain block step (gamma = 0) once fewer than gamma positions remain."""
+    cfg = VerifyConfig(0, "steps", "bf16", batch=6, num_q_heads=8, num_kv_heads=2,
+                       head_dim=128, prefix=(0, 300), block_size=8, max_ref=gamma,
+                       vocab=3000, plant=0.6, qkv_std=0.3, committed=committed)
+    inp = generate(cfg, seed=60 + 7 * gamma + committed, poison=True)
+    assert np.all(inp.num_ref == gamma)
+    assert np.all(np.sum(inp.step_map == 0, axis=1) == committed)
+    for chunk in (0, 64, -1):
+        _full_parity(inp, kv_chunk=chunk)
+
+
 @pytest.mark.parametrize("cid", [4, 5])
 def test_config_full_size_sampled(cid):
     """Full-size workloads in the benchmark's launch configuration; the oracle
