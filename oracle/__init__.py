@@ -10,6 +10,8 @@ A plain, slow, float64 numpy statement of what the GPU path computes:
   * ``accept``    the greedy (temperature-0) form of the acceptance rule of
                   eq. 2: argmax with lowest-index ties, softmax confidence, the
                   target probability of each draft and the accepted prefix length;
+  * ``rope``      rotary embedding at the RoPE-copy positions of Sec. 3.1-3.2,
+                  applied to the new slots' queries and keys when asked for;
   * ``sampled``   the stochastic form of eq. 2 at temperature T: acceptance with
                   probability min(1, p_theta/p_phi) from caller-supplied uniforms
                   and the residual draw at the first rejection.

@@ -9,7 +9,9 @@ Decoding and KV Cache").
 
 Grouped-query attention maps query head h to KV head h // (Hq // Hkv).
 Scores are scale * q.k with scale = 1/sqrt(d) unless given.  A padded row has no
-visible key: its output is 0 and its log-sum-exp is -inf.
+visible key: its output is 0 and its log-sum-exp is -inf.  With rope_theta > 0
+the new slots' queries and keys are rotated first, at the RoPE-copy positions
+of ``rope.positions`` (the cached prefix keys arrive rotated).
 """
 
 from __future__ import annotations
@@ -20,6 +22,7 @@ from typing import Iterable, Optional, Tuple
 import numpy as np
 
 from .mask import new_slot_visibility, row_valid
+from .rope import positions, rotate
 from .widen import widen
 
 
@@ -62,7 +65,7 @@ def prefix_kv(inp, b: int, kvh: int) -> Tuple[np.ndarray, np.ndarray]:
     return widen(kc, dt), widen(vc, dt)
 
 
-def pair_attention(inp, b: int, kvh: int, scale: Optional[float] = None):
+def pair_attention(inp, b: int, kvh: int, scale: Optional[float] = None, rope_theta: float = 0.0):
     """All rows of the G query heads sharing KV head kvh in sequence b.
 
     Returns out [n_new, G, d] and lse [G, n_new].
@@ -75,7 +78,11 @@ def pair_attention(inp, b: int, kvh: int, scale: Optional[float] = None):
     A = new_slot_visibility(inp.step_map[b], gamma, L)
     valid = row_valid(inp.step_map[b], gamma, L)
     kp, vp = prefix_kv(inp, b, kvh)
-    keys = np.concatenate([kp, widen(inp.k_new[b, :, kvh], dt)], axis=0)
+    kn = widen(inp.k_new[b, :, kvh], dt)
+    pos = positions(inp.step_map[b], gamma, L, int(inp.prefix_lens[b]))
+    if rope_theta:
+        kn = rotate(kn, pos, rope_theta)
+    keys = np.concatenate([kp, kn], axis=0)
     vals = np.concatenate([vp, widen(inp.v_new[b, :, kvh], dt)], axis=0)
     n_new = A.shape[0]
     vis = np.concatenate([np.repeat(valid[:, None], kp.shape[0], axis=1), A], axis=1)
@@ -83,14 +90,17 @@ def pair_attention(inp, b: int, kvh: int, scale: Optional[float] = None):
     lse = np.zeros((G, n_new))
     for g in range(G):
         h = kvh * G + g
-        o, l = attend(widen(inp.q[b, :, h], dt), keys, vals, vis, sc)
+        qh = widen(inp.q[b, :, h], dt)
+        if rope_theta:
+            qh = rotate(qh, pos, rope_theta)
+        o, l = attend(qh, keys, vals, vis, sc)
         out[:, g] = o
         lse[g] = l
     return out, lse
 
 
 def verify_attention(inp, scale: Optional[float] = None,
-                     pairs: Optional[Iterable[Tuple[int, int]]] = None):
+                     pairs: Optional[Iterable[Tuple[int, int]]] = None, rope_theta: float = 0.0):
     """Outputs of the verification attention.
 
     Returns out [batch, B+L, Hq, d] and lse [batch, Hq, B+L] (float64).  With
@@ -104,7 +114,7 @@ def verify_attention(inp, scale: Optional[float] = None,
     lse = np.full((b, Hq, n_new), np.nan)
     todo = pairs if pairs is not None else [(s, h) for s in range(b) for h in range(Hkv)]
     for s, kvh in todo:
-        o, l = pair_attention(inp, s, kvh, scale)
+        o, l = pair_attention(inp, s, kvh, scale, rope_theta)
         out[s, :, kvh * G:(kvh + 1) * G] = o
         lse[s, kvh * G:(kvh + 1) * G] = l
     return out, lse

@@ -169,3 +169,63 @@ def test_sampled_mutation_caught(monkeypatch, which):
     assert sampled_pins_ok()
     _sampled_variant(monkeypatch, which)
     assert not sampled_pins_ok()
+
+
+# ---- rotary embedding --------------------------------------------------------
+
+import test_oracle_rope as trope
+from oracle import rope as orope
+
+
+def rope_pins_ok():
+    try:
+        for d, th in [(2, 10000.0), (8, 10000.0), (64, 1e6), (128, 1e6)]:
+            trope.test_rotation_matches_complex_form(d, th)
+        trope.test_relative_positions_norms_identity()
+        trope.test_copy_positions_hand_example()
+        trope.test_attention_with_rope_equals_prerotated_inputs(3, 0)
+        trope.test_attention_with_rope_equals_prerotated_inputs(4, 4)
+        trope.test_verification_slot_sees_its_draft_at_distance_zero()
+    except AssertionError:
+        return False
+    return True
+
+
+@pytest.mark.parametrize("which", ["physical_positions", "interleaved_pairs", "half_frequency",
+                                   "prefix_rotated_again"])
+def test_rope_mutation_caught(monkeypatch, which):
+    assert rope_pins_ok()
+    if which == "physical_positions":
+        def phys(step_row, gamma, L, prefix_len):
+            return prefix_len + np.arange(len(step_row) + L)
+        monkeypatch.setattr(orope, "positions", phys)
+        monkeypatch.setattr(oattn, "positions", phys)
+    elif which == "interleaved_pairs":
+        def inter(x, pos, theta):
+            d = x.shape[-1]
+            ang = pos.astype(np.float64)[:, None] * orope.inv_freq(d, theta)[None, :]
+            c, s = np.cos(ang), np.sin(ang)
+            out = x.copy()
+            out[:, 0::2] = x[:, 0::2] * c - x[:, 1::2] * s
+            out[:, 1::2] = x[:, 1::2] * c + x[:, 0::2] * s
+            return out
+        monkeypatch.setattr(orope, "rotate", inter)
+        monkeypatch.setattr(oattn, "rotate", inter)
+    elif which == "half_frequency":
+        monkeypatch.setattr(orope, "inv_freq", lambda d, theta: theta ** (-1.0 * np.arange(d // 2) / d))
+    elif which == "prefix_rotated_again":
+        real_prefix = oattn.prefix_kv
+        real_pair = oattn.pair_attention
+
+        def pair(inp, b, kvh, scale=None, rope_theta=0.0):
+            if rope_theta:
+                def pk(inp_, b_, kvh_):
+                    k, v = real_prefix(inp_, b_, kvh_)
+                    return orope.rotate(k, np.arange(k.shape[0]), rope_theta), v
+                monkeypatch.setattr(oattn, "prefix_kv", pk)
+            try:
+                return real_pair(inp, b, kvh, scale, rope_theta)
+            finally:
+                monkeypatch.setattr(oattn, "prefix_kv", real_prefix)
+        monkeypatch.setattr(oattn, "pair_attention", pair)
+    assert not rope_pins_ok()
