@@ -73,7 +73,7 @@ def test_gqa_map_mutation_caught(monkeypatch):
     """Query head h must use KV head h // G, not h % Hkv."""
     real = oattn.pair_attention
 
-    def wrong(inp, b, kvh, scale=None):
+    def wrong(inp, b, kvh, scale=None, rope_theta=0.0):
         cfg = inp.cfg
         G, Hkv = cfg.group, cfg.num_kv_heads
         out = np.zeros((cfg.n_new, G, cfg.head_dim))
