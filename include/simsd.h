@@ -126,6 +126,10 @@ typedef struct {
   int64_t cache_stride_head;  /* elements between consecutive KV heads            */
   float scale;                /* softmax scale; 0 = 1/sqrt(head_dim)              */
   simsd_dtype dtype;          /* of q, k_new, v_new, k_cache, v_cache and out     */
+  float rope_theta;           /* 0: q and k_new arrive rotated.  > 0: they arrive
+                                 unrotated and the kernels apply the rotary
+                                 embedding with this base at the RoPE-copy
+                                 positions (see simsd_verify_attention)          */
 } simsd_attn_desc;
 
 /* Bytes of workspace simsd_verify_attention needs for `desc` (host only; 0 for
@@ -137,8 +141,9 @@ size_t simsd_verify_attention_workspace_size(const simsd_attn_desc* desc);
  * Verification"; mask: Sec. 3.1, eq. 1; the prompt is visible to every
  * non-padded response row, padding rows/columns are removed).
  *
- *   q       [batch, B+L, Hq,  head_dim]  queries of the new slots (after RoPE)
- *   k_new   [batch, B+L, Hkv, head_dim]  keys of the new slots (after RoPE)
+ *   q       [batch, B+L, Hq,  head_dim]  queries of the new slots (after RoPE,
+ *                                        or before it when rope_theta > 0)
+ *   k_new   [batch, B+L, Hkv, head_dim]  keys of the new slots (likewise)
  *   v_new   [batch, B+L, Hkv, head_dim]  values of the new slots
  *   k_cache, v_cache                     cached prefix, layout above
  *   block_table [batch, max_pages_per_seq] int32, or NULL if page_size == 0
@@ -153,6 +158,15 @@ size_t simsd_verify_attention_workspace_size(const simsd_attn_desc* desc);
  *                                        rows), or NULL
  *   workspace, workspace_bytes           see the conventions above
  *   stream                               hipStream_t
+ *
+ * RoPE copy (Sec. 3.1, Sec. 3.2), when rope_theta > 0: dims i and i + d/2 of
+ * each new slot's query and key are rotated by pos * rope_theta^(-2i/d), in
+ * fp32, before the scores (the new keys are rounded back to the input dtype).
+ * Block slot k sits at pos = prefix_lens[b] + k; reference slot r (draft r+1)
+ * shares the index of its verification slot, prefix_lens[b] + k_{r+1}, where
+ * step_map[b, k_{r+1}] = r + 1; padding reference slots take prefix_lens[b].
+ * The cached prefix keys must already be rotated at indices 0..prefix_len-1.
+ * rope_theta must be finite and >= 0 (SIMSD_ERR_BAD_SHAPE otherwise).
  */
 simsd_status simsd_verify_attention(const simsd_attn_desc* desc, const void* q,
                                     const void* k_new, const void* v_new,

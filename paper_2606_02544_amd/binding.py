@@ -31,7 +31,7 @@ class AttnDesc(ctypes.Structure):
                 ("max_pages_per_seq", ctypes.c_int32), ("kv_chunk", ctypes.c_int32),
                 ("cache_stride_seq", ctypes.c_int64), ("cache_stride_token", ctypes.c_int64),
                 ("cache_stride_head", ctypes.c_int64), ("scale", ctypes.c_float),
-                ("dtype", ctypes.c_int)]
+                ("dtype", ctypes.c_int), ("rope_theta", ctypes.c_float)]
 
 
 class AcceptDesc(ctypes.Structure):
@@ -136,7 +136,7 @@ WORKSPACES = _Workspaces()
 def attention_desc(q: torch.Tensor, k_cache: torch.Tensor, *, num_kv_heads: int,
                    block_size: int, max_ref: int, max_prefix_len: int, page_size: int = 0,
                    max_pages_per_seq: int = 0, kv_chunk: int = 0,
-                   scale: float = 0.0) -> AttnDesc:
+                   scale: float = 0.0, rope_theta: float = 0.0) -> AttnDesc:
     """Descriptor for q [batch, B+L, Hq, d] and a cache laid out as
     [batch, cap, Hkv, d] (contiguous) or [pages, page_size, Hkv, d] (paged)."""
     b, n_new, hq, d = q.shape
@@ -145,7 +145,8 @@ def attention_desc(q: torch.Tensor, k_cache: torch.Tensor, *, num_kv_heads: int,
                     block_size=block_size, max_ref=max_ref, max_prefix_len=max_prefix_len,
                     page_size=page_size, max_pages_per_seq=max_pages_per_seq,
                     kv_chunk=kv_chunk, cache_stride_seq=st[0], cache_stride_token=st[1],
-                    cache_stride_head=st[2], scale=scale, dtype=_dtype_code(q.dtype))
+                    cache_stride_head=st[2], scale=scale, dtype=_dtype_code(q.dtype),
+                    rope_theta=rope_theta)
 
 
 def attention_workspace_size(desc: AttnDesc) -> int:
@@ -159,6 +160,7 @@ def accept_workspace_size(desc: AcceptDesc) -> int:
 def verify_attention(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens, step_map,
                      num_ref, *, block_size: int, max_ref: int, max_prefix_len: int,
                      page_size: int = 0, kv_chunk: int = 0, scale: float = 0.0,
+                     rope_theta: float = 0.0,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      want_lse: bool = True, workspace: Optional[torch.Tensor] = None,
                      stream=None, desc: Optional[AttnDesc] = None):
@@ -169,7 +171,7 @@ def verify_attention(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens
                               page_size=page_size,
                               max_pages_per_seq=(block_table.shape[1]
                                                  if block_table is not None else 0),
-                              kv_chunk=kv_chunk, scale=scale)
+                              kv_chunk=kv_chunk, scale=scale, rope_theta=rope_theta)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:

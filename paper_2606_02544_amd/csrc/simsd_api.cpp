@@ -66,6 +66,9 @@ extern "C" simsd_status simsd_verify_attention(
     a.splits = p.splits;
     a.max_prefix = desc->max_prefix_len;
     a.scale_log2 = p.scale_log2;
+    a.rope = desc->rope_theta > 0.f ? 1 : 0;
+    a.rope_step = p.rope_step;
+    a.rope_theta = desc->rope_theta;
     const hipError_t e = launch_attention(*desc, p, a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "simsd_verify_attention launch");
     return SIMSD_OK;

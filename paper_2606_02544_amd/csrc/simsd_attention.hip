@@ -152,6 +152,29 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 // Two floats -> two bf16 (round to nearest even) in one instruction.
+// Rotary embedding (RoPE copy, Sec. 3.1-3.2).  Pair i of a head turns by
+// pos * 2^(i * step) radians; the angle is formed in revolutions so that the
+// hardware sine and cosine (period 1) apply after dropping whole turns.
+constexpr float kInv2Pi = 0.15915494309189535f;
+__device__ inline void rope_cs(int pos, int i, float step, float& c, float& s) {
+  const float rev = static_cast<float>(pos) * (__builtin_amdgcn_exp2f(static_cast<float>(i) * step) * kInv2Pi);
+  const float f = __builtin_amdgcn_fractf(rev);
+  s = __builtin_amdgcn_sinf(f);
+  c = __builtin_amdgcn_cosf(f);
+}
+
+// Positions of the new slots: block slot k at plen + k; reference slot r
+// (draft r + 1) at its verification slot's index; padding reference slots at
+// plen.  One wave; lane j holds block slot j's step.
+__device__ inline void build_positions(int* s_pos, int step, int gamma, int B, int L, int plen,
+                                       int lane) {
+  if (lane < L) s_pos[B + lane] = plen;
+  if (lane < B) {
+    s_pos[lane] = plen + lane;
+    if (step >= 1 && step <= gamma) s_pos[B + step - 1] = plen + lane;
+  }
+}
+
 __device__ inline uint32_t pack2(float lo, float hi) {
   const f32x2 v = {lo, hi};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
@@ -345,7 +368,7 @@ struct KVRing {
 // 8-wave groups have a CU to themselves (their registers allow no second
 // group) and keep three tiles in flight; 4-wave groups run two to a CU, each
 // with a two-tile ring (measured faster than one group with a deeper ring).
-template <int D, int RW, int KW, bool PAGED>
+template <int D, int RW, int KW, bool PAGED, bool ROPE>
 __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a, const Work& w) {
   constexpr int NW = RW * KW;
   constexpr int NBUF = NW >= 8 ? 4 : 2;
@@ -356,6 +379,7 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
   using Ring = KVRing<D, NW, PAGED>;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NBUF][2][TILEB];   // [slot][K, V]
   __shared__ uint64_t vis[kMaxNew];
+  __shared__ int s_pos[kMaxNew];               // rotary positions of the new slots
   __shared__ int s_pg_arr[PAGED ? kMaxChunkPages : 1];
   SIMSD_LDS int* s_pg = (SIMSD_LDS int*)(&s_pg_arr[0]);
 
@@ -411,8 +435,37 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
     if (j < nt) kv.issue(ring0 + j * kSlotBytes, tile_k0(j), j == ntp, w.kend, s_pg);
 
   build_visibility<NW>(vis, lane_step, w.gamma, a.B, a.n_new, wave, lane);
-  __syncthreads();                             // visibility words
+  if (ROPE && wave == 0) build_positions(s_pos, lane_step, w.gamma, a.B, a.L, w.plen, lane);
+  __syncthreads();                             // visibility words, positions
   const uint64_t myvis = row_in ? vis[t] : 0ull;
+  if constexpr (ROPE) {
+    // This lane's query dims 16*ks + 8*h + e (ks < KS/2) pair with the same
+    // offsets in ks + KS/2; both halves sit in this lane.
+    const int pos = s_pos[t];
+#pragma unroll
+    for (int ks = 0; ks < KS / 2; ++ks) {
+      u32x4 lo = __builtin_bit_cast(u32x4, qop[ks]), hi = __builtin_bit_cast(u32x4, qop[ks + KS / 2]);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        float x1[2], x2[2], y1[2], y2[2];
+        x1[0] = __uint_as_float(lo[p] << 16);
+        x1[1] = __uint_as_float(lo[p] & 0xffff0000u);
+        x2[0] = __uint_as_float(hi[p] << 16);
+        x2[1] = __uint_as_float(hi[p] & 0xffff0000u);
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          float c, sn;
+          rope_cs(pos, 16 * ks + 8 * h + 2 * p + e, a.rope_step, c, sn);
+          y1[e] = x1[e] * c - x2[e] * sn;
+          y2[e] = x2[e] * c + x1[e] * sn;
+        }
+        lo[p] = pack2(y1[0], y1[1]);
+        hi[p] = pack2(y2[0], y2[1]);
+      }
+      qop[ks] = __builtin_bit_cast(bf16x8, lo);
+      qop[ks + KS / 2] = __builtin_bit_cast(bf16x8, hi);
+    }
+  }
 
   f32x16 o[NB];
 #pragma unroll
@@ -464,6 +517,38 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
     // LDS-typed pointers (no generic-pointer arithmetic on the ring).
     const SIMSD_LDS uint8_t* sk = reinterpret_cast<const SIMSD_LDS uint8_t*>(ring0) + sl * kSlotBytes;
     const SIMSD_LDS uint8_t* sv = sk + TILEB;
+    if (ROPE && decltype(masked)::value && is_new) {
+      // Rotate the new keys in place: item (row r, chunk pair L) holds dims
+      // 8L..8L+7 and their partners 8L + D/2.. (16-byte chunks L and L + CH/2,
+      // swizzled).  Rows past the new slots hold copies of the last one.
+      constexpr int CH = D / 8;
+      SIMSD_LDS uint8_t* skw = const_cast<SIMSD_LDS uint8_t*>(sk);
+      for (int item = tid; item < kTile * (CH / 2); item += NW * 64) {
+        const int r = item / (CH / 2), L = item % (CH / 2);
+        const int pos = s_pos[min(r, a.n_new - 1)];
+        SIMSD_LDS u32x4* c1 = reinterpret_cast<SIMSD_LDS u32x4*>(skw + r * ROWB + 16 * (L ^ swz<D>(r)));
+        SIMSD_LDS u32x4* c2 = reinterpret_cast<SIMSD_LDS u32x4*>(skw + r * ROWB + 16 * ((L + CH / 2) ^ swz<D>(r)));
+        u32x4 lo = *c1, hi = *c2;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          float y1[2], y2[2];
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const float x1 = __uint_as_float(e ? (lo[p] & 0xffff0000u) : (lo[p] << 16));
+            const float x2 = __uint_as_float(e ? (hi[p] & 0xffff0000u) : (hi[p] << 16));
+            float c, sn;
+            rope_cs(pos, 8 * L + 2 * p + e, a.rope_step, c, sn);
+            y1[e] = x1 * c - x2 * sn;
+            y2[e] = x2 * c + x1 * sn;
+          }
+          lo[p] = pack2(y1[0], y1[1]);
+          hi[p] = pack2(y2[0], y2[1]);
+        }
+        *c1 = lo;
+        *c2 = hi;
+      }
+      __syncthreads();
+    }
 
     // The wave's key blocks of this tile, one at a time: both 32-key blocks
     // when KW == 1, block kw when KW == 2.  (Taking both blocks' scores at
@@ -636,11 +721,11 @@ __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a,
 
 // Chunked decomposition: one work-group per (prefix chunk, KV head x row
 // block, sequence).
-template <int D, int RW, int KW, bool PAGED>
+template <int D, int RW, int KW, bool PAGED, bool ROPE>
 __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_kernel(AttnArgs a) {
   Work w;
   if (!setup_work(a, w, D)) return;
-  attend_segment<D, RW, KW, PAGED>(a, w);
+  attend_segment<D, RW, KW, PAGED, ROPE>(a, w);
 }
 
 // Stream decomposition, for large and ragged batches.  The tiles of all
@@ -674,7 +759,7 @@ __device__ inline void stream_offsets(const AttnArgs& a, int64_t* seq0) {
   }
 }
 
-template <int D, int RW, int KW, bool PAGED>
+template <int D, int RW, int KW, bool PAGED, bool ROPE>
 __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_stream(AttnArgs a) {
   __shared__ int64_t seq0[kMaxStreamBatch + 1];
   stream_offsets(a, seq0);
@@ -720,7 +805,7 @@ __global__ void __launch_bounds__(RW * KW * 64, 2) attn_bf16_stream(AttnArgs a) 
     w.final = t0 == 0 && t1 == tp;
     w.part = a.part + (static_cast<int64_t>(g) * 2 + (x == lo ? 0 : 1)) *
                           static_cast<int64_t>(a.rows_pb) * (D + 2);
-    attend_segment<D, RW, KW, PAGED>(a, w);
+    attend_segment<D, RW, KW, PAGED, ROPE>(a, w);
     x += t1 - t0;
   }
 }
@@ -740,12 +825,29 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
   __shared__ float so[32 * D];
   __shared__ float sm[32], sl[32];
   __shared__ uint64_t vis[kMaxNew];
+  __shared__ int s_pos[kMaxNew];
 
   Work w;
   if (!setup_work(a, w, D)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* step_row = a.step_map + static_cast<int64_t>(w.b) * a.B;
-  build_visibility<NT / 64>(vis, step_row[min(lane, a.B - 1)], w.gamma, a.B, a.n_new, wave, lane);
+  const int lane_step = step_row[min(lane, a.B - 1)];
+  build_visibility<NT / 64>(vis, lane_step, w.gamma, a.B, a.n_new, wave, lane);
+  if (a.rope) {
+    if (wave == 0) build_positions(s_pos, lane_step, w.gamma, a.B, a.L, w.plen, lane);
+    __syncthreads();
+  }
+  // Rotary embedding of element e of a new slot's row x (fp64 angles: this is
+  // the exact path): dims e and e +- D/2 form the pair.
+  auto rotated = [&](const float* x, int e, int slot) -> float {
+    const float v = x[e];
+    if (!a.rope) return v;
+    const int i = e % (D / 2);
+    const float partner = x[e < D / 2 ? e + D / 2 : e - D / 2];
+    const double ang = static_cast<double>(s_pos[slot]) * pow(static_cast<double>(a.rope_theta), -2.0 * i / D);
+    const double c = cos(ang), sn = sin(ang);
+    return static_cast<float>(e < D / 2 ? v * c - partner * sn : v * c + partner * sn);
+  };
   if (tid < 32) {
     sm[tid] = kNegInf;
     sl[tid] = 0.f;
@@ -756,7 +858,7 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
     float v = 0.f;
     if (m < a.rows) {
       const int t = m / a.group, hq = w.kvh * a.group + m % a.group;
-      v = static_cast<const float*>(a.q)[((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D + d];
+      v = rotated(static_cast<const float*>(a.q) + ((static_cast<int64_t>(w.b) * a.n_new + t) * a.hq + hq) * D, d, t);
     }
     sq[idx] = v;
     so[idx] = 0.f;
@@ -776,9 +878,9 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
       if (is_new) {
         const int slot = k0 + row;
         if (slot < a.n_new) {
-          const int64_t off = ((static_cast<int64_t>(w.b) * a.n_new + slot) * a.hkv + w.kvh) * D + e;
-          kv = static_cast<const float*>(a.k_new)[off];
-          vv = static_cast<const float*>(a.v_new)[off];
+          const int64_t off = ((static_cast<int64_t>(w.b) * a.n_new + slot) * a.hkv + w.kvh) * D;
+          kv = rotated(static_cast<const float*>(a.k_new) + off, e, slot);
+          vv = static_cast<const float*>(a.v_new)[off + e];
         }
       } else if (k0 + row < w.kend) {
         const int64_t off = cache_offset<PAGED>(a, w.b, w.kvh, k0 + row, e);
@@ -980,21 +1082,29 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
         ok ? (mt + __log2f(lsum)) * kLn2 : kNegInf;
 }
 
-template <int D, bool PAGED>
-void launch_bf16(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st) {
+template <int D, bool PAGED, bool ROPE>
+void launch_bf16_variant(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st) {
   if (p.stream) {
     const dim3 sg(p.stream_groups);
     switch (p.row_waves) {
-      case 2: hipLaunchKernelGGL((attn_bf16_stream<D, 2, 2, PAGED>), sg, dim3(256), 0, st, a); break;
-      default: hipLaunchKernelGGL((attn_bf16_stream<D, 4, 2, PAGED>), sg, dim3(512), 0, st, a); break;
+      case 2: hipLaunchKernelGGL((attn_bf16_stream<D, 2, 2, PAGED, ROPE>), sg, dim3(256), 0, st, a); break;
+      default: hipLaunchKernelGGL((attn_bf16_stream<D, 4, 2, PAGED, ROPE>), sg, dim3(512), 0, st, a); break;
     }
     return;
   }
   switch (p.row_waves) {
-    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED>), grid, dim3(512), 0, st, a); break;
-    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED>), grid, dim3(512), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED, ROPE>), grid, dim3(256), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED, ROPE>), grid, dim3(512), 0, st, a); break;
+    default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED, ROPE>), grid, dim3(512), 0, st, a); break;
   }
+}
+
+// The rotary variants are separate instantiations: their extra registers stay
+// out of the kernels that run without it.
+template <int D, bool PAGED>
+void launch_bf16(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st) {
+  if (a.rope) launch_bf16_variant<D, PAGED, true>(p, grid, a, st);
+  else launch_bf16_variant<D, PAGED, false>(p, grid, a, st);
 }
 
 // Chunked merge: loads per round near the split count.

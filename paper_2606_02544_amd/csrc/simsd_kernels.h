@@ -28,6 +28,9 @@ struct AttnArgs {
   int page_size, max_pages, chunk, splits, max_prefix;
   int stream_groups;  // stream decomposition: work-groups (0 = chunked decomposition)
   float scale_log2;
+  int rope;           // rotary embedding of the new slots' q and k at the RoPE-copy positions
+  float rope_step;    // pair i turns by pos * exp2(i * rope_step)
+  float rope_theta;   // the base itself (the fp32 path forms its angles in fp64)
 };
 
 struct AcceptArgs {

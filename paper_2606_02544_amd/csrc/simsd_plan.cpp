@@ -60,6 +60,8 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   }
   if (!(std::isfinite(d->scale) && d->scale >= 0.f))
     return fail(SIMSD_ERR_BAD_SHAPE, "attention: scale must be finite and >= 0");
+  if (!(std::isfinite(d->rope_theta) && d->rope_theta >= 0.f))
+    return fail(SIMSD_ERR_BAD_SHAPE, "attention: rope_theta must be finite and >= 0");
 
   AttnPlan r;
   r.group = d->num_q_heads / d->num_kv_heads;
@@ -124,6 +126,8 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   }
   const float scale = d->scale > 0.f ? d->scale : 1.0f / std::sqrt(static_cast<float>(d->head_dim));
   r.scale_log2 = scale * 1.4426950408889634f;
+  // theta^(-2i/d) = exp2(i * rope_step), rope_step = -2 log2(theta) / d
+  r.rope_step = d->rope_theta > 0.f ? -2.0f * std::log2(d->rope_theta) / d->head_dim : 0.f;
   *p = r;
   return SIMSD_OK;
 }

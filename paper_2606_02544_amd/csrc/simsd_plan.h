@@ -37,6 +37,7 @@ struct AttnPlan {
   size_t part_floats = 0;   // floats per split partial: rows_pb * (head_dim + 2)
   size_t workspace = 0;     // total bytes
   float scale_log2 = 0.f;   // softmax scale * log2(e)
+  float rope_step = 0.f;    // rotary: log2 of the frequency ratio between pairs (0 = off)
 };
 
 struct AcceptPlan {

@@ -37,13 +37,14 @@ class DeviceInputs:
         self.draft_ids = int_tensor(inp.draft_ids, device)
 
 
-def run_attention(d: DeviceInputs, kv_chunk: int = 0):
+def run_attention(d: DeviceInputs, kv_chunk: int = 0, rope_theta: float = 0.0):
     from paper_2606_02544_amd import binding
     cfg = d.inp.cfg
     out, lse = binding.verify_attention(
         d.q, d.k_new, d.v_new, d.k_cache, d.v_cache, d.block_table, d.prefix_lens,
         d.step_map, d.num_ref, block_size=cfg.block_size, max_ref=cfg.max_ref,
-        max_prefix_len=cfg.max_prefix, page_size=cfg.page_size, kv_chunk=kv_chunk)
+        max_prefix_len=cfg.max_prefix, page_size=cfg.page_size, kv_chunk=kv_chunk,
+        rope_theta=rope_theta)
     torch.cuda.synchronize()
     return out.float().cpu().double().numpy(), lse.cpu().double().numpy()
 

@@ -114,7 +114,8 @@ def call_attention(desc, **over):
     ("kv_chunk", -64, 2), ("kv_chunk", -2, 2), ("page_size", -2, 2),
     ("stream_f32", -1, 3), ("stream_batch", -1, 3), ("stream_rows", -1, 3), ("cache_stride_token", 12, 4),
     ("cache_stride_head", -8, 2), ("scale", -1.0, 2), ("scale", float("inf"), 2),
-    ("dtype", 7, 3),
+    ("dtype", 7, 3), ("rope_theta", -1.0, 2), ("rope_theta", float("nan"), 2),
+    ("rope_theta", float("inf"), 2),
 ])
 def test_attention_descriptor_errors(field, value, status):
     desc = cfg_desc(2)
