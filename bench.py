@@ -87,7 +87,7 @@ def recorded_traffic(workload: str):
         return None
 
 
-def cpu_baseline(inp, seconds: float, outputs=None, sampled=None):
+def cpu_baseline(inp, seconds: float, outputs=None, sampled=None, rope_theta=0.0):
     """The oracle leg.  The oracle (float64 numpy) on the same workload,
     repeated whole steps until ``seconds`` have passed, or on a subset of
     (sequence, KV head) pairs plus their sequences' accept rows when one step
@@ -114,7 +114,7 @@ def cpu_baseline(inp, seconds: float, outputs=None, sampled=None):
         o = outputs["out"].float().cpu().double().numpy()
         l_ = outputs["lse"].cpu().double().numpy()
         pairs = [(0, 0), (b - 1, cfg.num_kv_heads - 1)]
-        ro, rl = oracle.verify_attention(inp, pairs=pairs)
+        ro, rl = oracle.verify_attention(inp, pairs=pairs, rope_theta=rope_theta)
         G = cfg.group
         ok = True
         for s_, h_ in pairs:
@@ -148,7 +148,7 @@ def cpu_baseline(inp, seconds: float, outputs=None, sampled=None):
     # one step: attention over all pairs, then the accept scan
     while time.perf_counter() - t0 < seconds:
         for (s, h) in pairs:
-            oracle.verify_attention(inp, pairs=[(s, h)])
+            oracle.verify_attention(inp, pairs=[(s, h)], rope_theta=rope_theta)
             done_pairs += 1
             tokens += per_pair_tokens
             if time.perf_counter() - t0 >= seconds:
@@ -193,6 +193,9 @@ def main():
     ap.add_argument("--gamma", type=int, default=None,
                     help="drafts per step (reference slots L = gamma <= B; default: the workload's); "
                          "0 = the plain block step once fewer than gamma positions remain")
+    ap.add_argument("--rope-theta", type=float, default=0.0,
+                    help="rotary base: q and the new keys arrive unrotated and the attention "
+                         "kernel rotates them at the RoPE-copy positions (0 = off)")
     ap.add_argument("--committed", type=int, default=0,
                     help="block slots already committed by earlier steps of the block")
     ap.add_argument("--no-graph", action="store_true",
@@ -221,7 +224,7 @@ def main():
     from synth import CONFIGS, generate, generate_draft_side
 
     cfg = CONFIGS[args.config]
-    custom = args.gamma is not None or args.committed
+    custom = args.gamma is not None or args.committed or args.rope_theta > 0
     if custom:
         import dataclasses
         g = cfg.max_ref if args.gamma is None else args.gamma
@@ -272,7 +275,7 @@ def main():
         base["q"], base["k_cache"], num_kv_heads=cfg.num_kv_heads, block_size=B, max_ref=L,
         max_prefix_len=cfg.max_prefix, page_size=cfg.page_size,
         max_pages_per_seq=0 if inp.block_table is None else inp.block_table.shape[1],
-        kv_chunk=args.kv_chunk)
+        kv_chunk=args.kv_chunk, rope_theta=args.rope_theta)
     cdesc = binding.accept_desc(base["logits"], L)
     aws_n = binding.attention_workspace_size(adesc)
     cws_n = (binding.accept_sampled_workspace_size(cdesc) if sampled
@@ -405,6 +408,7 @@ def main():
                         f"head_dim {cfg.head_dim}, prefix {cfg.prefix}, block {B}, "
                         f"{L} reference slots, vocab {cfg.vocab}"
                         + (f", gamma {L}, {cfg.committed} committed" if custom else "")
+                        + (f", RoPE base {args.rope_theta:g} fused" if args.rope_theta > 0 else "")
                         + (f", paged {cfg.page_size}" if cfg.page_size else ""),
             "step_hbm_bytes": step_bytes,
             "step_hbm_gbs": step_bytes / (elapsed / K) / 1e9,
@@ -435,7 +439,8 @@ def main():
         outputs = None if args.no_check else dict(out=out, lse=lse, tid=tid, alen=alen, corr=corr)
         line["cpu_baseline"], line["parity"] = cpu_baseline(
             inp, args.cpu_seconds, outputs,
-            sampled=(dlog_np, unif_np, args.temperature) if sampled else None)
+            sampled=(dlog_np, unif_np, args.temperature) if sampled else None,
+            rope_theta=args.rope_theta)
     print(json.dumps(line), flush=True)
 
 

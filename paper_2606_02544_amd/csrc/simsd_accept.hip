@@ -162,7 +162,7 @@ __global__ void __launch_bounds__(NT) scan_kernel(AcceptArgs a) {
   const int c = blockIdx.x, y = blockIdx.y, b = blockIdx.z;
   const int esz = BF16 ? 2 : 4;
   const char* row;
-  if (y < a.B) {
+  if (!SAMPLED || y < a.B) {                 // (greedy grids have B rows: no test)
     const int step = a.step_map[static_cast<int64_t>(b) * a.B + y];
     if (step < 1) return;                    // committed or padding: not scanned
     if (SAMPLED && step > min(max(a.num_ref[b], 0), a.L)) return;   // not drafted

@@ -34,25 +34,30 @@ struct AttnArgs {
 };
 
 struct AcceptArgs {
+  // Greedy and sampled (the greedy kernels read only this first block, so it
+  // stays small and in one place for their argument loads).
   const void* logits;
-  const void* draft_logits;   // sampled: [batch, L, V], same dtype as logits
   const int32_t* draft_ids;
   const int32_t* step_map;
   const int32_t* num_ref;
-  const float* uniforms;      // sampled: [batch, L + 1]
   int32_t* target_ids;
   float* confidence;
   float* draft_prob;          // greedy: target probability of each draft; sampled: p_theta(D_r)
-  float* p_draft;             // sampled: p_phi(D_r)
   int32_t* accept_len;
-  int32_t* correction;        // sampled: token drawn at the first rejection, or -1
   AcceptPartial* part;
-  DrawRow* draw_row;          // sampled: [batch]
-  DrawPartial* draw_part;     // sampled: [batch, draw_chunks]
-  int64_t nvec, chunk_vecs, draw_vecs;
-  int B, L, V, cpr, draw_chunks;
+  int64_t nvec, chunk_vecs;
+  int B, L, V, cpr;
   int rows;                   // partial rows per sequence: B, or B + L (sampled)
   float cl;                   // log2(e) / temperature
+  // Sampled only.
+  const void* draft_logits;   // [batch, L, V], same dtype as logits
+  const float* uniforms;      // [batch, L + 1]
+  float* p_draft;             // p_phi(D_r)
+  int32_t* correction;        // token drawn at the first rejection, or -1
+  DrawRow* draw_row;          // [batch]
+  DrawPartial* draw_part;     // [batch, draw_chunks]
+  int64_t draw_vecs;
+  int draw_chunks;
 };
 
 hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const AttnArgs& a,
