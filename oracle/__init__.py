@@ -12,6 +12,8 @@ A plain, slow, float64 numpy statement of what the GPU path computes:
                   target probability of each draft and the accepted prefix length;
   * ``rope``      rotary embedding at the RoPE-copy positions of Sec. 3.1-3.2,
                   applied to the new slots' queries and keys when asked for;
+  * ``lmhead``    the verification logits written out as hidden . weight^T
+                  (float64) and handed to the greedy acceptance;
   * ``sampled``   the stochastic form of eq. 2 at temperature T: acceptance with
                   probability min(1, p_theta/p_phi) from caller-supplied uniforms
                   and the residual draw at the first rejection.
@@ -28,6 +30,8 @@ from .mask import slot_labels, new_slot_visibility, DATA, MASK
 from .attention import attend, verify_attention
 from .accept import verify_accept
 from .sampled import verify_accept_sampled
+from .lmhead import lmhead_logits, verify_accept_lmhead
 
 __all__ = ["widen", "slot_labels", "new_slot_visibility", "DATA", "MASK", "attend",
-           "verify_attention", "verify_accept", "verify_accept_sampled"]
+           "verify_attention", "verify_accept", "verify_accept_sampled", "lmhead_logits",
+           "verify_accept_lmhead"]

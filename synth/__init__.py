@@ -7,7 +7,8 @@ and the GPU path both consume what it produces and neither is imported here.
 """
 
 from .configs import CONFIGS, VerifyConfig, config_by_id
-from .generate import VerifyInputs, generate, generate_draft_side, bf16_bits_from_f32
+from .generate import (VerifyInputs, generate, generate_draft_side, generate_lmhead_side,
+                       bf16_bits_from_f32)
 
 __all__ = ["CONFIGS", "VerifyConfig", "config_by_id", "VerifyInputs", "generate",
-           "generate_draft_side", "bf16_bits_from_f32"]
+           "generate_draft_side", "generate_lmhead_side", "bf16_bits_from_f32"]

@@ -303,3 +303,45 @@ def generate_draft_side(inp: VerifyInputs, corr: float = 0.8,
     u = np.random.default_rng(s_u).random((b, L + 1)).astype(np.float32)
     np.minimum(u, np.nextafter(np.float32(1), np.float32(0)), out=u)
     return draft_logits, u
+
+
+def generate_lmhead_side(inp: VerifyInputs, hidden_size: int, threads: Optional[int] = None):
+    """Final hidden states and LM-head weight for `inp`, in its dtype.
+
+    Returns (hidden [batch, B, H], weight [V, H]).  weight ~ N(0, logit_std^2 / H)
+    so that logits = hidden . weight^T have the workload's spread for
+    hidden ~ N(0, 1).  For a planted draft (``inp.planted``) the hidden state of
+    its verification row is pulled towards the draft's weight row:
+    h = 0.5 * noise + (6.25 * logit_std / |w_D|^2) * w_D, which puts the draft's
+    logit near 6.25 sigma (no logit or maximum is computed here).  From child
+    stream 11 of the sequence's SeedSequence.
+    """
+    cfg = inp.cfg
+    b, B, V, H = cfg.batch, cfg.block_size, cfg.vocab, hidden_size
+    s_lm = np.random.default_rng(np.random.SeedSequence(inp.seed_entropy).spawn(12)[11])
+    wstd = np.float32(cfg.logit_std / np.sqrt(H))
+    bf16 = cfg.dtype != "f32"
+    weight = np.empty((V, H), np.uint16 if bf16 else np.float32)
+    step = 1 << 13
+    streams = s_lm.bit_generator.seed_seq.spawn((V + step - 1) // step + 1)
+
+    def wjob(i):                                  # bounded float32 temporaries
+        v0 = i * step
+        x = np.random.default_rng(streams[i]).standard_normal((min(step, V - v0), H), dtype=np.float32)
+        x *= wstd
+        weight[v0:v0 + step] = bf16_bits_from_f32(x) if bf16 else x
+
+    nthreads = threads or min(16, os.cpu_count() or 1)
+    with cf.ThreadPoolExecutor(max_workers=nthreads) as ex:
+        list(ex.map(wjob, range((V + step - 1) // step)))
+    hidden = np.random.default_rng(streams[-1]).standard_normal((b, B, H), dtype=np.float32)
+    as_f32 = (lambda a: (a.astype(np.uint32) << 16).view(np.float32)) if bf16 else (lambda a: a)
+    for s in range(b):
+        for r in range(int(inp.num_ref[s])):
+            if not inp.planted[s, r]:
+                continue
+            k = int(np.flatnonzero(inp.step_map[s] == r + 1)[0])
+            w = as_f32(weight[int(inp.draft_ids[s, r])])
+            hidden[s, k] = np.float32(0.5) * hidden[s, k] + \
+                np.float32(6.25 * cfg.logit_std / float(np.dot(w, w))) * w
+    return (bf16_bits_from_f32(hidden) if bf16 else hidden), weight
