@@ -262,6 +262,43 @@ simsd_status simsd_verify_accept_sampled(const simsd_accept_desc* desc, float te
                                          size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* LM head fused with the scan                                                */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t batch;             /* sequences, >= 1                                    */
+  int32_t block_size;        /* B, 1 <= B <= 64                                    */
+  int32_t max_ref;           /* L, 0 <= L <= B                                     */
+  int32_t vocab;             /* V >= 1                                             */
+  int32_t hidden;            /* H, a positive multiple of 64                       */
+  simsd_dtype dtype;         /* of hidden and weight: SIMSD_BF16 only              */
+} simsd_lmhead_desc;
+
+size_t simsd_verify_accept_lmhead_workspace_size(const simsd_lmhead_desc* desc);
+
+/*
+ * Greedy verification as simsd_verify_accept, with the logits computed on
+ * the fly from the verification rows' final hidden states and the LM-head
+ * weight (the target model's prediction at each verification slot, Sec. 3.2):
+ * logits[b, k, v] = hidden[b, k, :] . weight[v, :], accumulated in fp32 from
+ * bf16 products, never stored.  Outputs and their meaning are those of
+ * simsd_verify_accept (ties between exactly equal fp32 logits go to the lowest
+ * index).
+ *
+ *   hidden  [batch, B, H] bf16, 16-byte aligned; row k = block slot k
+ *   weight  [V, H] bf16, 16-byte aligned (a Linear layer's [out, in] layout)
+ *   draft_ids, step_map, num_ref, target_ids, confidence, draft_prob,
+ *   accept_len, workspace, workspace_bytes, stream   as for simsd_verify_accept
+ * The workspace must hold simsd_verify_accept_lmhead_workspace_size() bytes.
+ */
+simsd_status simsd_verify_accept_lmhead(const simsd_lmhead_desc* desc, const void* hidden,
+                                        const void* weight, const int32_t* draft_ids,
+                                        const int32_t* step_map, const int32_t* num_ref,
+                                        int32_t* target_ids, float* confidence, float* draft_prob,
+                                        int32_t* accept_len, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Host-only helpers (no GPU needed)                                          */
 /* ------------------------------------------------------------------------ */
 

@@ -40,6 +40,12 @@ class AcceptDesc(ctypes.Structure):
                 ("chunks_per_row", ctypes.c_int32), ("logits_dtype", ctypes.c_int)]
 
 
+class LmheadDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("max_ref", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("hidden", ctypes.c_int32), ("dtype", ctypes.c_int)]
+
+
 class SimsdError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{STATUS.get(status, status)}: {message}")
@@ -73,6 +79,11 @@ def lib() -> ctypes.CDLL:
         L.simsd_verify_accept_sampled.argtypes = [ctypes.POINTER(AcceptDesc), ctypes.c_float] + \
             [_P] * 10 + [_P, ctypes.c_size_t, _P]
         L.simsd_verify_accept_sampled.restype = ctypes.c_int
+        L.simsd_verify_accept_lmhead_workspace_size.argtypes = [ctypes.POINTER(LmheadDesc)]
+        L.simsd_verify_accept_lmhead_workspace_size.restype = ctypes.c_size_t
+        L.simsd_verify_accept_lmhead.argtypes = [ctypes.POINTER(LmheadDesc)] + [_P] * 9 + \
+            [_P, ctypes.c_size_t, _P]
+        L.simsd_verify_accept_lmhead.restype = ctypes.c_int
         L.simsd_validate_step_map.argtypes = [_I32P, _I32P, ctypes.c_int32, ctypes.c_int32,
                                               ctypes.c_int32]
         L.simsd_validate_step_map.restype = ctypes.c_int
@@ -253,6 +264,44 @@ def verify_accept_sampled(logits, draft_logits, draft_ids, step_map, num_ref, un
         _ptr(p_draft), _ptr(accept_len), _ptr(correction), _ptr(workspace), ws_bytes,
         _stream(stream)))
     return p_target, p_draft, accept_len, correction
+
+
+def lmhead_desc(hidden: torch.Tensor, weight: torch.Tensor, max_ref: int) -> LmheadDesc:
+    b, B, H = hidden.shape
+    return LmheadDesc(batch=b, block_size=B, max_ref=max_ref, vocab=weight.shape[0], hidden=H,
+                      dtype=_dtype_code(hidden.dtype))
+
+
+def lmhead_workspace_size(desc: LmheadDesc) -> int:
+    return int(lib().simsd_verify_accept_lmhead_workspace_size(ctypes.byref(desc)))
+
+
+def verify_accept_lmhead(hidden, weight, draft_ids, step_map, num_ref, *, target_ids=None,
+                         confidence=None, draft_prob=None, accept_len=None, workspace=None,
+                         stream=None, desc: Optional[LmheadDesc] = None):
+    """simsd_verify_accept_lmhead on torch tensors (hidden [b, B, H], weight [V, H]).
+    Returns (target_ids, confidence, draft_prob, accept_len)."""
+    b, B, H = hidden.shape
+    L = draft_ids.shape[1]
+    if desc is None:
+        desc = lmhead_desc(hidden, weight, L)
+    dev = hidden.device
+    if target_ids is None:
+        target_ids = torch.empty((b, B), dtype=torch.int32, device=dev)
+    if confidence is None:
+        confidence = torch.empty((b, B), dtype=torch.float32, device=dev)
+    if draft_prob is None:
+        draft_prob = torch.empty((b, L), dtype=torch.float32, device=dev)
+    if accept_len is None:
+        accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
+    if workspace is None:
+        workspace = WORKSPACES.get(dev, "lmhead", lmhead_workspace_size(desc))
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().simsd_verify_accept_lmhead(
+        ctypes.byref(desc), _ptr(hidden), _ptr(weight), _ptr(draft_ids), _ptr(step_map),
+        _ptr(num_ref), _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
+        _ptr(workspace), ws_bytes, _stream(stream)))
+    return target_ids, confidence, draft_prob, accept_len
 
 
 def validate_step_map(step_map, num_ref, max_ref: int):

@@ -9,7 +9,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = ["simsd_attention.hip", "simsd_accept.hip", "simsd_api.cpp", "simsd_plan.cpp"]
+SOURCES = ["simsd_attention.hip", "simsd_accept.hip", "simsd_lmhead.hip", "simsd_api.cpp",
+           "simsd_plan.cpp"]
 OUT = os.path.join(HERE, "libsimsd.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -262,7 +262,9 @@ __device__ inline void merge_rows(const AcceptArgs& a, int nr, int wave, int lan
 
 // One work-group per sequence: merge the chunks of every row, then the
 // per-row outputs, draft probabilities and the accepted-prefix length.
-template <bool BF16>
+// LMHEAD: the logits were never stored; the scan left each drafted token's
+// logit in a.xdraft.
+template <bool BF16, bool LMHEAD = false>
 __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
   constexpr int NWV = NT / 64;
   __shared__ Best s_row[kMaxNew];
@@ -308,8 +310,10 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
   float x = 0.f;
   if (wave == 0 && r < gamma) {
     kr = s_row_of_step[r];
-    if (kr >= 0 && tok >= 0 && tok < a.V)
-      x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
+    if (kr >= 0 && tok >= 0 && tok < a.V) {
+      if (LMHEAD) x = a.xdraft[static_cast<int64_t>(b) * a.L + r];
+      else x = load_elem<BF16>(logits_b + static_cast<int64_t>(kr) * a.V * esz, tok);
+    }
   }
 
   if (mode == 1) merge_packed(a, a.B, wave, lane, lg, rpw, buf, s_row);
@@ -685,6 +689,11 @@ hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const 
   if (e != hipSuccess) return e;
   if (bf16) hipLaunchKernelGGL((finalize_kernel<true>), dim3(d.batch), block, 0, st, a);
   else hipLaunchKernelGGL((finalize_kernel<false>), dim3(d.batch), block, 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_finalize_lmhead(int batch, const AcceptArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((finalize_kernel<true, true>), dim3(batch), dim3(NT), 0, st, a);
   return hipGetLastError();
 }
 

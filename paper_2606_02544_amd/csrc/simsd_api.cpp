@@ -118,6 +118,67 @@ extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const
   }
 }
 
+extern "C" size_t simsd_verify_accept_lmhead_workspace_size(const simsd_lmhead_desc* desc) {
+  LmheadPlan p;
+  if (plan_lmhead(desc, lmhead_vocab_tile(), lmhead_stage(), &p) != SIMSD_OK) return 0;
+  return p.workspace;
+}
+
+extern "C" simsd_status simsd_verify_accept_lmhead(
+    const simsd_lmhead_desc* desc, const void* hidden, const void* weight,
+    const int32_t* draft_ids, const int32_t* step_map, const int32_t* num_ref,
+    int32_t* target_ids, float* confidence, float* draft_prob, int32_t* accept_len,
+    void* workspace, size_t workspace_bytes, void* stream) {
+  try {
+    LmheadPlan p;
+    simsd_status st = plan_lmhead(desc, lmhead_vocab_tile(), lmhead_stage(), &p);
+    if (st != SIMSD_OK) return st;
+    st = check_lmhead_args(desc, p, hidden, weight, draft_ids, step_map, num_ref, target_ids,
+                           accept_len, workspace, workspace_bytes);
+    if (st != SIMSD_OK) return st;
+    float* xdraft = reinterpret_cast<float*>(static_cast<char*>(workspace) + p.xdraft_off);
+    LmheadArgs l{};
+    l.hidden = hidden;
+    l.weight = weight;
+    l.draft_ids = draft_ids;
+    l.step_map = step_map;
+    l.num_ref = num_ref;
+    l.part = static_cast<AcceptPartial*>(workspace);
+    l.xdraft = xdraft;
+    l.R = desc->batch * desc->block_size;
+    l.B = desc->block_size;
+    l.L = desc->max_ref;
+    l.V = desc->vocab;
+    l.H = desc->hidden;
+    l.vtiles = p.vtiles;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_lmhead_scan(l, s);
+    if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept_lmhead launch");
+    AcceptArgs a{};
+    a.draft_ids = draft_ids;
+    a.step_map = step_map;
+    a.num_ref = num_ref;
+    a.target_ids = target_ids;
+    a.confidence = confidence;
+    a.draft_prob = draft_prob;
+    a.accept_len = accept_len;
+    a.part = static_cast<AcceptPartial*>(workspace);
+    a.B = desc->block_size;
+    a.L = desc->max_ref;
+    a.V = desc->vocab;
+    a.cpr = p.vtiles;
+    a.rows = desc->block_size;
+    a.cl = kLog2eHost;
+    a.xdraft = xdraft;
+    e = launch_finalize_lmhead(desc->batch, a, s);
+    if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept_lmhead launch");
+    return SIMSD_OK;
+  } catch (...) {
+    set_error("simsd_verify_accept_lmhead: internal error");
+    return SIMSD_ERR_HIP;
+  }
+}
+
 extern "C" simsd_status simsd_verify_accept_sampled(
     const simsd_accept_desc* desc, float temperature, const void* logits, const void* draft_logits,
     const int32_t* draft_ids, const int32_t* step_map, const int32_t* num_ref,

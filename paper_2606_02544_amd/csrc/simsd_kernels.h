@@ -58,6 +58,19 @@ struct AcceptArgs {
   DrawPartial* draw_part;     // [batch, draw_chunks]
   int64_t draw_vecs;
   int draw_chunks;
+  const float* xdraft;        // LM-head path: the drafted tokens' logits [batch, L]
+};
+
+// LM-head product fused with the vocabulary scan.
+struct LmheadArgs {
+  const void* hidden;         // [R = batch * B, H] bf16
+  const void* weight;         // [V, H] bf16
+  const int32_t* draft_ids;
+  const int32_t* step_map;
+  const int32_t* num_ref;
+  AcceptPartial* part;        // [R, vtiles]
+  float* xdraft;              // [batch, L]
+  int R, B, L, V, H, vtiles;
 };
 
 hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const AttnArgs& a,
@@ -66,5 +79,9 @@ hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const 
                          hipStream_t stream);
 hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p,
                                  const AcceptArgs& a, hipStream_t stream);
+hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t stream);
+hipError_t launch_finalize_lmhead(int batch, const AcceptArgs& a, hipStream_t stream);
+int lmhead_vocab_tile();   // vocabulary entries per scan work-group
+int lmhead_stage();        // reduction elements per stage (H must be a multiple)
 
 }  // namespace simsd

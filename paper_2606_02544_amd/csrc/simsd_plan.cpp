@@ -227,6 +227,51 @@ simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
   return SIMSD_OK;
 }
 
+simsd_status plan_lmhead(const simsd_lmhead_desc* d, int vocab_tile, int stage, LmheadPlan* p) {
+  if (!d || !p) return fail(SIMSD_ERR_NULL_POINTER, "lmhead: descriptor is NULL");
+  if (d->dtype != SIMSD_BF16) return fail(SIMSD_ERR_UNSUPPORTED, "lmhead: dtype must be SIMSD_BF16");
+  if (d->batch < 1 || d->batch > 65535)
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: batch must be in [1, 65535]");
+  if (d->block_size < 1 || d->block_size > kMaxNew)
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: block_size must be in [1, 64]");
+  if (d->max_ref < 0 || d->max_ref > d->block_size)
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: need 0 <= max_ref <= block_size");
+  if (d->vocab < 1) return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: vocab must be >= 1");
+  if (d->hidden < stage || d->hidden % stage != 0)
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: hidden must be a positive multiple of 64");
+  if (static_cast<int64_t>(d->batch) * d->block_size > (int64_t{1} << 24) ||
+      static_cast<int64_t>(d->vocab) * d->hidden * 2 > (int64_t{1} << 40))
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: sizes too large");
+  LmheadPlan r;
+  r.vtiles = static_cast<int>(ceil_div(d->vocab, vocab_tile));
+  if (r.vtiles > 65535) return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: vocab too large");
+  const size_t parts = static_cast<size_t>(d->batch) * d->block_size * r.vtiles * sizeof(AcceptPartial);
+  r.xdraft_off = (parts + 255) / 256 * 256;
+  r.workspace = r.xdraft_off + static_cast<size_t>(d->batch) * std::max(d->max_ref, 1) * sizeof(float);
+  *p = r;
+  return SIMSD_OK;
+}
+
+simsd_status check_lmhead_args(const simsd_lmhead_desc* d, const LmheadPlan& p, const void* hidden,
+                               const void* weight, const int32_t* draft_ids,
+                               const int32_t* step_map, const int32_t* num_ref,
+                               const int32_t* target_ids, const int32_t* accept_len,
+                               const void* workspace, size_t workspace_bytes) {
+  if (!hidden || !weight || !step_map || !num_ref || !target_ids || !accept_len)
+    return fail(SIMSD_ERR_NULL_POINTER,
+                "lmhead: hidden, weight, step_map, num_ref, target_ids and accept_len are required");
+  if (d->max_ref > 0 && !draft_ids)
+    return fail(SIMSD_ERR_NULL_POINTER, "lmhead: draft_ids required when max_ref > 0");
+  if (!aligned16(hidden) || !aligned16(weight))
+    return fail(SIMSD_ERR_ALIGNMENT, "lmhead: hidden and weight must be 16-byte aligned");
+  if (!workspace) return fail(SIMSD_ERR_WORKSPACE, "lmhead: workspace is NULL");
+  if (!aligned16(workspace)) return fail(SIMSD_ERR_ALIGNMENT, "lmhead: workspace must be 16-byte aligned");
+  if (workspace_bytes < p.workspace)
+    return fail(SIMSD_ERR_WORKSPACE,
+                "lmhead: workspace smaller than simsd_verify_accept_lmhead_workspace_size()");
+  return SIMSD_OK;
+}
+
 simsd_status check_accept_sampled_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                        float temperature, const void* logits,
                                        const void* draft_logits, const int32_t* draft_ids,

@@ -62,6 +62,12 @@ struct AcceptPartial {
   int32_t pad;
 };
 
+struct LmheadPlan {
+  int vtiles = 0;         // vocabulary tiles (scan work-groups per row tile)
+  size_t xdraft_off = 0;  // workspace offset (bytes) of the drafted tokens' logits
+  size_t workspace = 0;
+};
+
 // Sampled rule: what the draw needs of one sequence (written once the
 // acceptance is decided; acc >= gamma, kr = -1 when every draft was accepted).
 struct DrawRow {
@@ -94,6 +100,12 @@ simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const int32_t* step_map, const int32_t* num_ref,
                                const int32_t* target_ids, const float* confidence,
                                const float* draft_prob, const int32_t* accept_len,
+                               const void* workspace, size_t workspace_bytes);
+simsd_status plan_lmhead(const simsd_lmhead_desc* d, int vocab_tile, int stage, LmheadPlan* p);
+simsd_status check_lmhead_args(const simsd_lmhead_desc* d, const LmheadPlan& p, const void* hidden,
+                               const void* weight, const int32_t* draft_ids,
+                               const int32_t* step_map, const int32_t* num_ref,
+                               const int32_t* target_ids, const int32_t* accept_len,
                                const void* workspace, size_t workspace_bytes);
 simsd_status check_accept_sampled_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                        float temperature, const void* logits,

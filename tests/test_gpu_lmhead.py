@@ -1,0 +1,63 @@
+"""GPU parity of the LM head fused with the vocabulary scan against the oracle
+(logits = hidden . weight^T in float64, then the greedy acceptance), through
+the C ABI.  The kernel accumulates fp32 from bf16 products: a target id may
+differ from the oracle's only where the oracle's top two logits lie within
+1e-4 of each other (checked for validity instead); accept lengths follow the
+target ids; confidence and draft probabilities within 1e-4 relative."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import dev_tensor, int_tensor
+from synth import VerifyConfig, config_by_id, generate, generate_lmhead_side
+
+pytestmark = pytest.mark.gpu
+
+
+def run_lmhead(inp, hidden, weight):
+    from paper_2606_02544_amd import binding
+    t, c, p, a = binding.verify_accept_lmhead(
+        dev_tensor(hidden, "bf16"), dev_tensor(weight, "bf16"), int_tensor(inp.draft_ids),
+        int_tensor(inp.step_map), int_tensor(inp.num_ref))
+    torch.cuda.synchronize()
+    return t.cpu().numpy(), c.cpu().double().numpy(), p.cpu().double().numpy(), a.cpu().numpy()
+
+
+def check_lmhead(inp, hidden, weight, got):
+    t, c, p, a = got
+    rt, rc, rp, ra, logits = oracle.verify_accept_lmhead(hidden, weight, inp.draft_ids,
+                                                         inp.step_map, inp.num_ref, "bf16")
+    scanned = inp.step_map >= 1
+    near = 0
+    for s, k in zip(*np.nonzero(scanned)):
+        if t[s, k] != rt[s, k]:
+            row = logits[s, k]
+            assert 0 <= t[s, k] < row.size and row.max() - row[t[s, k]] <= 1e-4 * max(1.0, abs(row.max())), \
+                (s, k, t[s, k], rt[s, k])
+            near += 1
+    assert np.all(t[~scanned] == -1)
+    if near == 0:
+        np.testing.assert_array_equal(a, ra)
+    np.testing.assert_allclose(c, rc, rtol=1e-4, atol=1e-30)
+    np.testing.assert_allclose(p, rp, rtol=1e-4, atol=1e-30)
+
+
+LMHEAD_CASES = [
+    # batch, B, L, V, H, step_mode, seed: ragged vocabulary and row tiles, mixed step maps
+    (3, 8, 6, 1000, 256, "mixed", 1),
+    (5, 16, 16, 2051, 512, "full", 2),
+    (9, 32, 24, 777, 128, "mixed", 3),       # 288 rows: three row tiles
+    (1, 4, 4, 151936, 2048, "full", 4),      # SDAR-1.7B-shaped head
+]
+
+
+@pytest.mark.parametrize("case", LMHEAD_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_lmhead_parity(case):
+    b, B, L, V, H, mode, seed = case
+    cfg = VerifyConfig(0, "lmhead", "bf16", batch=b, num_q_heads=2, num_kv_heads=1, head_dim=64,
+                       prefix=4, block_size=B, max_ref=L, vocab=V, plant=0.6, step_mode=mode)
+    inp = generate(cfg, seed=seed, bad_draft_rate=0.2 if mode == "mixed" else 0.0)
+    hidden, weight = generate_lmhead_side(inp, H)
+    check_lmhead(inp, hidden, weight, run_lmhead(inp, hidden, weight))
