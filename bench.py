@@ -87,7 +87,7 @@ def recorded_traffic(workload: str):
         return None
 
 
-def cpu_baseline(inp, seconds: float, outputs=None, sampled=None, rope_theta=0.0):
+def cpu_baseline(inp, seconds: float, outputs=None, sampled=None, rope_theta=0.0, lmhead=None):
     """The oracle leg.  The oracle (float64 numpy) on the same workload,
     repeated whole steps until ``seconds`` have passed, or on a subset of
     (sequence, KV head) pairs plus their sequences' accept rows when one step
@@ -97,6 +97,10 @@ def cpu_baseline(inp, seconds: float, outputs=None, sampled=None, rope_theta=0.0
     import oracle
 
     def accept_oracle(sl):
+        if lmhead is not None:
+            hidden, weight = lmhead
+            return oracle.verify_accept_lmhead(hidden[sl], weight, inp.draft_ids[sl],
+                                               inp.step_map[sl], inp.num_ref[sl], inp.cfg.dtype)[:4]
         if sampled is None:
             return oracle.verify_accept(inp.logits[sl], inp.draft_ids[sl], inp.step_map[sl],
                                         inp.num_ref[sl], inp.cfg.dtype)
@@ -190,6 +194,11 @@ def main():
     ap.add_argument("--accept", choices=["greedy", "sampled"], default="greedy",
                     help="acceptance rule: greedy (eq. 2 at T = 0) or sampled (eq. 2 at --temperature)")
     ap.add_argument("--temperature", type=float, default=1.0)
+    ap.add_argument("--lmhead", action="store_true",
+                    help="greedy acceptance from the final hidden states and the LM-head weight "
+                         "(logits never stored) instead of from stored logits")
+    ap.add_argument("--hidden", type=int, default=0,
+                    help="LM-head hidden size (default: 2048 for the SDAR-1.7B layer, else 4096)")
     ap.add_argument("--gamma", type=int, default=None,
                     help="drafts per step (reference slots L = gamma <= B; default: the workload's); "
                          "0 = the plain block step once fewer than gamma positions remain")
@@ -221,7 +230,7 @@ def main():
         print(json.dumps({"copy_probe_bytes": n, "launches": 5}))
         return
     from paper_2606_02544_amd import binding
-    from synth import CONFIGS, generate, generate_draft_side
+    from synth import CONFIGS, generate, generate_draft_side, generate_lmhead_side
 
     cfg = CONFIGS[args.config]
     custom = args.gamma is not None or args.committed or args.rope_theta > 0
@@ -236,8 +245,16 @@ def main():
     print(f"[bench] generating {cfg.name}", file=sys.stderr, flush=True)
     inp = generate(cfg)
     sampled = args.accept == "sampled"
+    if sampled and args.lmhead:
+        sys.exit("--lmhead computes the greedy rule; it does not combine with --accept sampled")
     dlog_np, unif_np = generate_draft_side(inp) if sampled else (None, None)
+    H = args.hidden or (2048 if cfg.name == "sdar-1.7b-layer" else 4096)
+    hid_np, w_np = generate_lmhead_side(inp, H) if args.lmhead else (None, None)
     wl = workload_numbers(inp, sampled)
+    if args.lmhead:
+        # the head's weight once, the rows' hidden states; flops of the product
+        wl["accept_bytes"] = cfg.vocab * H * 2 + cfg.batch * cfg.block_size * H * 2
+        wl["lmhead_flops"] = 2 * cfg.batch * cfg.block_size * cfg.vocab * H
     step_bytes = wl["attn_bytes"] + wl["accept_bytes"]
     copies = max(1, math.ceil(args.rotate_mb * 1e6 / step_bytes))
     copies = min(copies, max(1, int(40e9 // step_bytes)))
@@ -256,6 +273,10 @@ def main():
                 prefix_lens=to_dev(inp.prefix_lens, "i32"), step_map=to_dev(inp.step_map, "i32"),
                 num_ref=to_dev(inp.num_ref, "i32"), logits=to_dev(inp.logits, dt),
                 draft_ids=to_dev(inp.draft_ids, "i32"))
+    if args.lmhead:
+        del base["logits"]
+        base["hidden"] = to_dev(hid_np, dt)
+        base["weight"] = to_dev(w_np, dt)
     if sampled:
         base["draft_logits"] = to_dev(dlog_np, dt)
         base["uniforms"] = torch.from_numpy(unif_np).to(dev)
@@ -276,9 +297,11 @@ def main():
         max_prefix_len=cfg.max_prefix, page_size=cfg.page_size,
         max_pages_per_seq=0 if inp.block_table is None else inp.block_table.shape[1],
         kv_chunk=args.kv_chunk, rope_theta=args.rope_theta)
-    cdesc = binding.accept_desc(base["logits"], L)
+    cdesc = (binding.lmhead_desc(base["hidden"], base["weight"], L) if args.lmhead
+             else binding.accept_desc(base["logits"], L))
     aws_n = binding.attention_workspace_size(adesc)
     cws_n = (binding.accept_sampled_workspace_size(cdesc) if sampled
+             else binding.lmhead_workspace_size(cdesc) if args.lmhead
              else binding.accept_workspace_size(cdesc))
     aws = torch.zeros(max(aws_n, 16), dtype=torch.uint8, device=dev)
     cws = torch.zeros(max(cws_n, 16), dtype=torch.uint8, device=dev)
@@ -301,6 +324,10 @@ def main():
                           ptr(s["draft_logits"]), ptr(s["draft_ids"]), ptr(s["step_map"]),
                           ptr(s["num_ref"]), ptr(s["uniforms"]), ptr(dprob), ptr(pdraft),
                           ptr(alen), ptr(corr), ptr(cws), cws_n, sp)
+            elif args.lmhead:
+                c_args = (ctypes.byref(cdesc), ptr(s["hidden"]), ptr(s["weight"]),
+                          ptr(s["draft_ids"]), ptr(s["step_map"]), ptr(s["num_ref"]), ptr(tid),
+                          ptr(conf), ptr(dprob), ptr(alen), ptr(cws), cws_n, sp)
             else:
                 c_args = (ctypes.byref(cdesc), ptr(s["logits"]), ptr(s["draft_ids"]),
                           ptr(s["step_map"]), ptr(s["num_ref"]), ptr(tid), ptr(conf), ptr(dprob),
@@ -310,7 +337,8 @@ def main():
 
     calls = build_calls(torch.cuda.current_stream())
     f_attn = lib.simsd_verify_attention
-    f_acc = lib.simsd_verify_accept_sampled if sampled else lib.simsd_verify_accept
+    f_acc = (lib.simsd_verify_accept_sampled if sampled else
+             lib.simsd_verify_accept_lmhead if args.lmhead else lib.simsd_verify_accept)
 
     def launch_step(i, what=("attn", "acc")):
         a_args, c_args = calls[i % len(calls)]
@@ -416,12 +444,16 @@ def main():
             "attention_us": attn_ms * 1e3,
             "accept_us": acc_ms * 1e3,
             "accept_gbs": wl["accept_bytes"] / (acc_ms * 1e-3) / 1e9,
+            **({"lmhead_tflops": wl["lmhead_flops"] / (acc_ms * 1e-3) / 1e12,
+                "lmhead_mfma_frac": wl["lmhead_flops"] / (acc_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS}
+               if args.lmhead else {}),
             "scanned_rows_per_s": wl["scanned_rows"] * K / elapsed,
             "attention_mfma_frac": wl["attn_flops"] / (attn_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
             "input_copies": copies,
             "hip_graph": use_graph,
             "kv_chunk": args.kv_chunk,
-            "accept_rule": f"sampled, temperature {args.temperature}" if sampled else "greedy",
+            "accept_rule": (f"sampled, temperature {args.temperature}" if sampled else
+                            f"greedy, LM head fused (hidden {H})" if args.lmhead else "greedy"),
         },
         "roofline": {
             "bound": "hbm",
@@ -440,7 +472,7 @@ def main():
         line["cpu_baseline"], line["parity"] = cpu_baseline(
             inp, args.cpu_seconds, outputs,
             sampled=(dlog_np, unif_np, args.temperature) if sampled else None,
-            rope_theta=args.rope_theta)
+            rope_theta=args.rope_theta, lmhead=(hid_np, w_np) if args.lmhead else None)
     print(json.dumps(line), flush=True)
 
 

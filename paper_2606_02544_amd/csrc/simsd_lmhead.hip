@@ -12,12 +12,13 @@
 // for the draft probability.  finalize_kernel (simsd_accept.hip) then merges
 // the partials and finds the accepted prefix as for stored logits.
 //
-// Tiles: 128 rows x 256 vocabulary entries per 8-wave work-group; wave w
-// covers rows 64*(w/4).. and vocabulary 64*(w%4).. (2 x 2 MFMA blocks).  The
-// reduction dimension streams in 64-wide stages through two LDS buffers
-// (register-staged loads of stage s+1 overlap the MFMAs of stage s); rows are
-// padded to 144 bytes so the 16-byte operand reads of 32 rows hit distinct
-// banks.
+// Tiles: TR rows x TV vocabulary entries per 8-wave work-group; wave w covers
+// rows (TR/2)*(w/4).. and vocabulary (TV/4)*(w%4).. in 32 x 32 MFMA blocks.  The
+// reduction dimension streams in KS-wide stages through a ring of NBUF LDS
+// stages filled by direct global-to-LDS loads, so several stages are in
+// flight without staging registers.  A stage row holds CPR 16-byte chunks;
+// chunk c of row r sits at position c ^ swz(r), so the operand reads of 16
+// consecutive rows touch 64 distinct banks.
 #include "simsd_kernels.h"
 
 namespace simsd {
@@ -30,14 +31,22 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kNoIndex = 0x7fffffff;
-constexpr int NT = 512;                  // 8 waves
-constexpr int TR = 128;                  // rows per tile
+constexpr int NT = 512;                  // 8 waves: 4 vocabulary quarters x 2 row halves
 constexpr int TV = 256;                  // vocabulary entries per tile
-constexpr int KS = 64;                   // reduction elements per stage
-constexpr int PITCH = KS * 2 + 16;       // LDS bytes per row (padded)
-constexpr int CPR = KS * 2 / 16;         // 16-byte chunks per row per stage
-constexpr int WCH = TV * CPR / NT;       // weight chunks per thread per stage
-constexpr int HCH = TR * CPR / NT;       // hidden chunks per thread per stage
+constexpr int VBW = TV / 128;            // 32-entry MFMA blocks per wave
+
+#define LM_LDS __attribute__((address_space(3)))
+
+// 16 bytes per lane from a per-lane address into LDS at m0 + 16 * lane.
+__device__ inline void dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 struct Best {
   float mx;
@@ -56,95 +65,129 @@ __device__ inline Best combine(Best a, Best b) {
   return r;
 }
 
+// TR rows per tile, KS reduction elements per stage, NBUF stages in the ring.
+template <int TR, int KS, int NBUF>
 __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t s_w[2][TV * PITCH];
-  __shared__ __attribute__((aligned(16))) uint8_t s_h[2][TR * PITCH];
+  constexpr int RBW = TR / 64;             // 32-row MFMA blocks per wave
+  constexpr int CPR = KS / 8;              // 16-byte chunks per row per stage
+  constexpr int ROWB = KS * 2;             // LDS bytes per row per stage
+  constexpr int RPS = 16 / CPR;            // rows spanning the 64 banks
+  constexpr int STAGEB = (TV + TR) * ROWB; // one stage: weight rows, then hidden rows
+  constexpr int INSN = STAGEB / 1024;      // 1 KB direct loads per stage
+  constexpr int PERW = INSN / (NT / 64);   // per wave
+  constexpr int RPI = 64 / CPR;            // rows per direct load
+  static_assert(RBW >= 1 && TR % 64 == 0, "wave grid");
+  static_assert(KS % 16 == 0 && CPR <= 16, "stage width");
+  static_assert(INSN % (NT / 64) == 0, "stage loads split evenly over the waves");
+  static_assert(NBUF >= 2 && NBUF <= 5, "ring depth");
+  auto swz = [](int r) { return (r / RPS) % CPR; };
+  __shared__ __attribute__((aligned(1024))) uint8_t s_ring[NBUF][STAGEB];
   __shared__ Best s_part[4][TR];          // per vocabulary quarter, per row of the tile
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
   const int rw = wave / 4, vq = wave % 4;
-  const int r0 = blockIdx.x * TR, v0 = blockIdx.y * TV;
+  // Work-groups go to the eight XCDs round-robin.  Tile t = xcd * per + j
+  // (row tiles fastest) keeps the row tiles of one vocabulary tile on one XCD,
+  // whose L2 then serves them the weight tile once; ids past the last tile
+  // (grid padded to a multiple of 8) leave at once.
+  const int rtiles = (a.R + TR - 1) / TR, ntiles = rtiles * a.vtiles;
+  const int per = (ntiles + 7) / 8;
+  const int t = static_cast<int>(blockIdx.x % 8) * per + static_cast<int>(blockIdx.x / 8);
+  if (t >= ntiles) return;
+  const int vt = t / rtiles;
+  const int r0 = (t % rtiles) * TR, v0 = vt * TV;
   const int64_t rowb = static_cast<int64_t>(a.H) * 2;   // bytes per hidden / weight row
 
-  // This thread's chunks of each stage: chunk c = tid + NT*i covers row c/CPR,
-  // bytes 16*(c%CPR) of the stage.  Rows past the end read the last row.
-  const char* gw[WCH];
-  const char* gh[HCH];
-  uint32_t lw[WCH], lh[HCH];
+  // Instruction g = wave * PERW + i of a stage moves stage rows RPI*g ..
+  // RPI*g + RPI-1 (weight rows first, then hidden rows); lane l takes row
+  // RPI*g + l/CPR, chunk position l%CPR, i.e. logical chunk (l%CPR) ^ swz(row).
+  // Rows past the end read the last row (their results are dropped).
+  const char* src[PERW];
+  uint32_t dst[PERW];
 #pragma unroll
-  for (int i = 0; i < WCH; ++i) {
-    const int c = tid + NT * i, r = c / CPR, q = c % CPR;
-    gw[i] = static_cast<const char*>(a.weight) + min(v0 + r, a.V - 1) * rowb + 16 * q;
-    lw[i] = r * PITCH + 16 * q;
+  for (int i = 0; i < PERW; ++i) {
+    const int g = wave * PERW + i, r = RPI * g + lane / CPR;
+    const int c = (lane % CPR) ^ swz(r);
+    const char* rowp = r < TV
+        ? static_cast<const char*>(a.weight) + min(v0 + r, a.V - 1) * rowb
+        : static_cast<const char*>(a.hidden) + min(r0 + r - TV, a.R - 1) * rowb;
+    src[i] = rowp + 16 * c;
+    dst[i] = 1024u * g;
   }
-#pragma unroll
-  for (int i = 0; i < HCH; ++i) {
-    const int c = tid + NT * i, r = c / CPR, q = c % CPR;
-    gh[i] = static_cast<const char*>(a.hidden) + min(r0 + r, a.R - 1) * rowb + 16 * q;
-    lh[i] = r * PITCH + 16 * q;
-  }
-  u32x4 rw_[WCH], rh_[HCH];
-  auto load_stage = [&](int s) __attribute__((always_inline)) {
+  const uint32_t ring0 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (LM_LDS void*)(&s_ring[0][0])));
+  auto issue = [&](int s) __attribute__((always_inline)) {
     const int64_t off = static_cast<int64_t>(s) * KS * 2;
+    const uint32_t slot = ring0 + (s % NBUF) * STAGEB;
 #pragma unroll
-    for (int i = 0; i < WCH; ++i) rw_[i] = *reinterpret_cast<const u32x4*>(gw[i] + off);
-#pragma unroll
-    for (int i = 0; i < HCH; ++i) rh_[i] = *reinterpret_cast<const u32x4*>(gh[i] + off);
-  };
-  auto store_stage = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int i = 0; i < WCH; ++i) *reinterpret_cast<u32x4*>(&s_w[buf][lw[i]]) = rw_[i];
-#pragma unroll
-    for (int i = 0; i < HCH; ++i) *reinterpret_cast<u32x4*>(&s_h[buf][lh[i]]) = rh_[i];
+    for (int i = 0; i < PERW; ++i) dma16(src[i] + off, slot + dst[i]);
   };
 
-  f32x16 acc[2][2];                        // [vocab block][row block]
+  f32x16 acc[VBW][RBW];                    // [vocab block][row block]
 #pragma unroll
-  for (int vb = 0; vb < 2; ++vb)
+  for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < RBW; ++rb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) acc[vb][rb][j] = 0.f;
 
+  // Operand reads: row n of a 32-row block, logical chunk 2*ks + h.
+  constexpr int KSUB = KS / 16;
+  int ao[KSUB][VBW], bo[KSUB][RBW];
+#pragma unroll
+  for (int ks = 0; ks < KSUB; ++ks) {
+#pragma unroll
+    for (int vb = 0; vb < VBW; ++vb) {
+      const int rv = (TV / 4) * vq + 32 * vb + n;
+      ao[ks][vb] = rv * ROWB + 16 * ((2 * ks + h) ^ swz(rv));
+    }
+#pragma unroll
+    for (int rb = 0; rb < RBW; ++rb) {
+      const int rr = TV + (TR / 2) * rw + 32 * rb + n;
+      bo[ks][rb] = rr * ROWB + 16 * ((2 * ks + h) ^ swz(rr));
+    }
+  }
+
   const int S = a.H / KS;
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < NBUF - 1; ++s)
+    if (s < S) issue(s);
   for (int s = 0; s < S; ++s) {
-    const int buf = s & 1;
-    if (s + 1 < S) load_stage(s + 1);
-    const uint8_t* bw = s_w[buf];
-    const uint8_t* bh = s_h[buf];
+    // Stages issued: 0 .. min(S, s + NBUF - 1) - 1; stage s has landed once
+    // at most the younger ones remain.
+    const int younger = min(S, s + NBUF - 1) - 1 - s;
+    if (NBUF > 4 && younger >= 3) wait_vm<3 * PERW>();
+    else if (NBUF > 3 && younger >= 2) wait_vm<2 * PERW>();
+    else if (NBUF > 2 && younger >= 1) wait_vm<PERW>();
+    else wait_vm<0>();
+    lds_barrier();                         // stage s is in; stage s - 1's slot is free
+    if (s + NBUF - 1 < S) issue(s + NBUF - 1);
+    const LM_LDS uint8_t* st = reinterpret_cast<const LM_LDS uint8_t*>(ring0) + (s % NBUF) * STAGEB;
 #pragma unroll
-    for (int ks = 0; ks < KS / 16; ++ks) {
-      const int co = 32 * ks + 16 * h;     // bytes of reduction elements 16*ks + 8*h ..
-      bf16x8 fa[2], fb[2];
+    for (int ks = 0; ks < KSUB; ++ks) {
+      bf16x8 fa[VBW], fb[RBW];
 #pragma unroll
-      for (int vb = 0; vb < 2; ++vb)
-        fa[vb] = *reinterpret_cast<const bf16x8*>(bw + (64 * vq + 32 * vb + n) * PITCH + co);
+      for (int vb = 0; vb < VBW; ++vb) fa[vb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + ao[ks][vb]);
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
-        fb[rb] = *reinterpret_cast<const bf16x8*>(bh + (64 * rw + 32 * rb + n) * PITCH + co);
+      for (int rb = 0; rb < RBW; ++rb) fb[rb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + bo[ks][rb]);
 #pragma unroll
-      for (int vb = 0; vb < 2; ++vb)
+      for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int rb = 0; rb < RBW; ++rb)
           acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[vb], fb[rb], acc[vb][rb], 0, 0, 0);
     }
-    if (s + 1 < S) store_stage(buf ^ 1);
-    __syncthreads();
   }
 
   // Epilogue.  Register j of acc[vb][rb] holds vocabulary entry
-  // v0 + 64*vq + 32*vb + 8*(j/4) + 4*h + j%4 of row r0 + 64*rw + 32*rb + n.
+  // v0 + (TV/4)*vq + 32*vb + 8*(j/4) + 4*h + j%4 of row r0 + (TR/2)*rw + 32*rb + n.
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
-    const int rowl = 64 * rw + 32 * rb + n, row = r0 + rowl;
+  for (int rb = 0; rb < RBW; ++rb) {
+    const int rowl = (TR / 2) * rw + 32 * rb + n, row = r0 + rowl;
     // The drafted token of this row, if it is a verification row.
     int tok = -1, slot = -1;
     if (row < a.R) {
-      const int b = row / a.B, k = row % a.B;
+      const int b = row / a.B;
       const int step = a.step_map[row];
       const int gamma = min(max(a.num_ref[b], 0), a.L);
       if (step >= 1 && step <= gamma) {
@@ -155,10 +198,10 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     float mx = kNegInf;
     int ix = kNoIndex;
 #pragma unroll
-    for (int vb = 0; vb < 2; ++vb)
+    for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const int v = v0 + 64 * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
+        const int v = v0 + (TV / 4) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
         const float x = acc[vb][rb][j];
         if (v < a.V) {
           if (x > mx || (x == mx && v < ix)) {
@@ -171,10 +214,10 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     float sm = 0.f;
     if (mx != kNegInf) {
 #pragma unroll
-      for (int vb = 0; vb < 2; ++vb)
+      for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int v = v0 + 64 * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
+          const int v = v0 + (TV / 4) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
           if (v < a.V) sm += __builtin_amdgcn_exp2f((acc[vb][rb][j] - mx) * kLog2e);
         }
     }
@@ -196,19 +239,33 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     pr.ix = r.ix;
     pr.sm = r.sm;
     pr.pad = 0;
-    a.part[static_cast<int64_t>(r0 + tid) * a.vtiles + blockIdx.y] = pr;
+    a.part[static_cast<int64_t>(r0 + tid) * a.vtiles + vt] = pr;
   }
 }
 
 }  // namespace
 
-hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t st) {
-  const dim3 grid((a.R + TR - 1) / TR, a.vtiles);
-  hipLaunchKernelGGL(lmhead_scan_kernel, grid, dim3(NT), 0, st, a);
+namespace {
+template <int TR, int KS, int NBUF>
+hipError_t launch_variant(const LmheadArgs& a, hipStream_t st) {
+  const int ntiles = (a.R + TR - 1) / TR * a.vtiles;
+  hipLaunchKernelGGL((lmhead_scan_kernel<TR, KS, NBUF>), dim3((ntiles + 7) / 8 * 8), dim3(NT), 0,
+                     st, a);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t st) {
+  // Few rows: the weight stream is all there is; 72 KB of LDS lets two
+  // work-groups share a CU.  Up to one row tile: 128-byte row segments, one
+  // work-group per CU.  More rows: 256-row tiles halve the weight re-reads and
+  // the LDS reads per MFMA.
+  if (a.R <= 32) return launch_variant<128, 32, 3>(a, st);
+  if (a.R <= 128) return launch_variant<128, 64, 3>(a, st);
+  return launch_variant<256, 64, 2>(a, st);
 }
 
 int lmhead_vocab_tile() { return TV; }
-int lmhead_stage() { return KS; }
+int lmhead_stage() { return 64; }   // the widest stage of the variants
 
 }  // namespace simsd

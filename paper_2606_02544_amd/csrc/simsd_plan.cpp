@@ -245,6 +245,9 @@ simsd_status plan_lmhead(const simsd_lmhead_desc* d, int vocab_tile, int stage, 
   LmheadPlan r;
   r.vtiles = static_cast<int>(ceil_div(d->vocab, vocab_tile));
   if (r.vtiles > 65535) return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: vocab too large");
+  // The scan's tile count (row tiles x vocabulary tiles) stays an int.
+  if (static_cast<int64_t>(d->batch) * d->block_size * r.vtiles > (int64_t{1} << 30))
+    return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: batch * block_size * vocabulary tiles too large");
   const size_t parts = static_cast<size_t>(d->batch) * d->block_size * r.vtiles * sizeof(AcceptPartial);
   r.xdraft_off = (parts + 255) / 256 * 256;
   r.workspace = r.xdraft_off + static_cast<size_t>(d->batch) * std::max(d->max_ref, 1) * sizeof(float);

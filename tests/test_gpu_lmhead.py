@@ -45,11 +45,18 @@ def check_lmhead(inp, hidden, weight, got):
 
 
 LMHEAD_CASES = [
-    # batch, B, L, V, H, step_mode, seed: ragged vocabulary and row tiles, mixed step maps
+    # batch, B, L, V, H, step_mode, seed: ragged vocabulary and row tiles, mixed step
+    # maps.  Rows R = batch * B pick the kernel variant: R <= 32 (32-wide stages),
+    # R <= 128 (64-wide stages), more (256-row tiles, two-stage ring).
     (3, 8, 6, 1000, 256, "mixed", 1),
     (5, 16, 16, 2051, 512, "full", 2),
-    (9, 32, 24, 777, 128, "mixed", 3),       # 288 rows: three row tiles
+    (9, 32, 24, 777, 128, "mixed", 3),       # 288 rows: two 256-row tiles
     (1, 4, 4, 151936, 2048, "full", 4),      # SDAR-1.7B-shaped head
+    (2, 8, 8, 3000, 64, "mixed", 5),         # one reduction stage
+    (4, 16, 12, 1500, 192, "full", 6),       # as many stages as the ring holds
+    (6, 16, 8, 900, 64, "mixed", 7),         # 96 rows, one stage
+    (10, 16, 16, 1200, 64, "mixed", 8),      # 160 rows, one stage
+    (20, 32, 32, 2500, 320, "full", 9),      # 640 rows: three row tiles, odd stage count
 ]
 
 
