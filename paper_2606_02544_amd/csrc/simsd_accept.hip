@@ -320,11 +320,22 @@ __global__ void __launch_bounds__(NT) finalize_kernel(AcceptArgs a) {
   else if (mode == 2) merge_rows<2>(a, a.B, wave, lane, buf, s_row);
   else if (mode == 4) merge_rows<4>(a, a.B, wave, lane, buf, s_row);
   else {
+    // Many partials per row (the LM-head scan leaves one per vocabulary
+    // tile): eight independent loads per lane in flight, then their merge.
+    constexpr int U = 8;
     for (int kk = wave; kk < a.B; kk += NWV) {
       Best rr = {kNegInf, kNoIndex, 0.f};
-      for (int cc = lane; cc < a.cpr; cc += 64) {
-        const AcceptPartial pr = pb[static_cast<int64_t>(kk) * a.cpr + cc];
-        rr = combine(rr, Best{pr.mx, pr.ix, pr.sm}, a.cl);
+      const AcceptPartial* prow = pb + static_cast<int64_t>(kk) * a.cpr;
+      for (int c0 = 0; c0 < a.cpr; c0 += 64 * U) {
+        AcceptPartial v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int cc = c0 + 64 * u + lane;
+          if (cc < a.cpr) v[u] = prow[cc];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (c0 + 64 * u + lane < a.cpr) rr = combine(rr, Best{v[u].mx, v[u].ix, v[u].sm}, a.cl);
       }
       rr = wave_reduce(rr, a.cl);
       if (lane == 0) s_row[kk] = rr;

@@ -250,7 +250,7 @@ def test_accept_bench_shape_chunking():
     inp = generate(CONFIGS[2], seed=11)
     d = DeviceInputs(inp)
     ref = oracle_accept(inp)
-    for cpr in (1, 7, 64, 0):
+    for cpr in (1, 7, 64, 600, 1500, 0):     # 600, 1500: the long-row merge
         check_accept(run_accept(d, cpr), ref)
 
 
