@@ -144,6 +144,7 @@ extern "C" simsd_status simsd_verify_accept_lmhead(
     l.step_map = step_map;
     l.num_ref = num_ref;
     l.part = static_cast<AcceptPartial*>(workspace);
+    l.merged = reinterpret_cast<AcceptPartial*>(static_cast<char*>(workspace) + p.merged_off);
     l.xdraft = xdraft;
     l.R = desc->batch * desc->block_size;
     l.B = desc->block_size;
@@ -153,6 +154,7 @@ extern "C" simsd_status simsd_verify_accept_lmhead(
     l.vtiles = p.vtiles;
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e = launch_lmhead_scan(l, s);
+    if (e == hipSuccess) e = launch_lmhead_merge(l, s);
     if (e != hipSuccess) return hip_fail(e, "simsd_verify_accept_lmhead launch");
     AcceptArgs a{};
     a.draft_ids = draft_ids;
@@ -162,11 +164,11 @@ extern "C" simsd_status simsd_verify_accept_lmhead(
     a.confidence = confidence;
     a.draft_prob = draft_prob;
     a.accept_len = accept_len;
-    a.part = static_cast<AcceptPartial*>(workspace);
+    a.part = l.merged;
     a.B = desc->block_size;
     a.L = desc->max_ref;
     a.V = desc->vocab;
-    a.cpr = p.vtiles;
+    a.cpr = 1;
     a.rows = desc->block_size;
     a.cl = kLog2eHost;
     a.xdraft = xdraft;

@@ -69,6 +69,7 @@ struct LmheadArgs {
   const int32_t* step_map;
   const int32_t* num_ref;
   AcceptPartial* part;        // [R, vtiles]
+  AcceptPartial* merged;      // [R]: the partials of each row merged
   float* xdraft;              // [batch, L]
   int R, B, L, V, H, vtiles;
 };
@@ -80,6 +81,7 @@ hipError_t launch_accept(const simsd_accept_desc& d, const AcceptPlan& p, const 
 hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p,
                                  const AcceptArgs& a, hipStream_t stream);
 hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t stream);
+hipError_t launch_lmhead_merge(const LmheadArgs& a, hipStream_t st);
 hipError_t launch_finalize_lmhead(int batch, const AcceptArgs& a, hipStream_t stream);
 int lmhead_vocab_tile();   // vocabulary entries per scan work-group
 int lmhead_stage();        // reduction elements per stage (H must be a multiple)

@@ -9,8 +9,9 @@
 // vocabulary tile to (max, lowest index reaching it, sum of exp(x - max)) in
 // the epilogue, the partial the logits scan writes, so the logits never reach
 // memory.  The tile that holds a row's drafted token also stores that logit
-// for the draft probability.  finalize_kernel (simsd_accept.hip) then merges
-// the partials and finds the accepted prefix as for stored logits.
+// for the draft probability.  lmhead_merge_kernel merges each row's partials
+// (one wave per row) and finalize_kernel (simsd_accept.hip) finds the accepted
+// prefix from them as for stored logits.
 //
 // Tiles: TR rows x TV vocabulary entries per 8-wave work-group; wave w covers
 // rows (TR/2)*(w/4).. and vocabulary (TV/4)*(w%4).. in 32 x 32 MFMA blocks.  The
@@ -243,6 +244,42 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   }
 }
 
+// One wave per row merges the row's partials, one per vocabulary tile, so the
+// finalize kernel (one work-group per sequence) reads a single partial per row.
+__global__ void __launch_bounds__(NT) lmhead_merge_kernel(LmheadArgs a) {
+  constexpr int U = 8;                     // loads per lane in flight
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
+  if (row >= a.R) return;
+  const AcceptPartial* pr = a.part + static_cast<int64_t>(row) * a.vtiles;
+  Best r = {kNegInf, kNoIndex, 0.f};
+  for (int c0 = 0; c0 < a.vtiles; c0 += 64 * U) {
+    AcceptPartial v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c0 + 64 * u + lane < a.vtiles) v[u] = pr[c0 + 64 * u + lane];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c0 + 64 * u + lane < a.vtiles) r = combine(r, Best{v[u].mx, v[u].ix, v[u].sm});
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    Best o;
+    o.mx = __shfl_xor(r.mx, off);
+    o.ix = __shfl_xor(r.ix, off);
+    o.sm = __shfl_xor(r.sm, off);
+    r = combine(r, o);
+  }
+  if (lane == 0) {
+    AcceptPartial m;
+    m.mx = r.mx;
+    m.ix = r.ix;
+    m.sm = r.sm;
+    m.pad = 0;
+    a.merged[row] = m;
+  }
+}
+
 }  // namespace
 
 namespace {
@@ -263,6 +300,11 @@ hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t st) {
   if (a.R <= 32) return launch_variant<128, 32, 3>(a, st);
   if (a.R <= 128) return launch_variant<128, 64, 3>(a, st);
   return launch_variant<256, 64, 2>(a, st);
+}
+
+hipError_t launch_lmhead_merge(const LmheadArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(lmhead_merge_kernel, dim3((a.R + NT / 64 - 1) / (NT / 64)), dim3(NT), 0, st, a);
+  return hipGetLastError();
 }
 
 int lmhead_vocab_tile() { return TV; }

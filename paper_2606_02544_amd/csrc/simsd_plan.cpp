@@ -249,7 +249,9 @@ simsd_status plan_lmhead(const simsd_lmhead_desc* d, int vocab_tile, int stage, 
   if (static_cast<int64_t>(d->batch) * d->block_size * r.vtiles > (int64_t{1} << 30))
     return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: batch * block_size * vocabulary tiles too large");
   const size_t parts = static_cast<size_t>(d->batch) * d->block_size * r.vtiles * sizeof(AcceptPartial);
-  r.xdraft_off = (parts + 255) / 256 * 256;
+  r.merged_off = (parts + 255) / 256 * 256;
+  r.xdraft_off = (r.merged_off + static_cast<size_t>(d->batch) * d->block_size * sizeof(AcceptPartial) +
+                  255) / 256 * 256;
   r.workspace = r.xdraft_off + static_cast<size_t>(d->batch) * std::max(d->max_ref, 1) * sizeof(float);
   *p = r;
   return SIMSD_OK;

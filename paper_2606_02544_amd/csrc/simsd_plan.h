@@ -64,6 +64,7 @@ struct AcceptPartial {
 
 struct LmheadPlan {
   int vtiles = 0;         // vocabulary tiles (scan work-groups per row tile)
+  size_t merged_off = 0;  // workspace offset (bytes) of the merged per-row partials
   size_t xdraft_off = 0;  // workspace offset (bytes) of the drafted tokens' logits
   size_t workspace = 0;
 };
