@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from paper_2606_02544_amd import binding
-from paper_2606_02544_amd.binding import AttnDesc, AcceptDesc
+from paper_2606_02544_amd.binding import LmheadDesc, AttnDesc, AcceptDesc
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "simsd.h")
@@ -218,6 +218,41 @@ def test_accept_sampled_errors_and_workspace():
     # with L = 0 the draft inputs may be NULL
     d0 = AcceptDesc(**dict(good, max_ref=0))
     assert call_accept_sampled(d0, draft_logits=None, draft_ids=None, ws=0) in (0, 5)
+
+
+def call_lmhead(desc, **over):
+    _no_gpu()
+    a = dict(hidden=FAKE, weight=FAKE, draft_ids=FAKE, step_map=FAKE, num_ref=FAKE,
+             target_ids=FAKE, confidence=None, draft_prob=None, accept_len=FAKE, workspace=FAKE,
+             ws=1 << 30)
+    a.update(over)
+    return binding.lib().simsd_verify_accept_lmhead(
+        ctypes.byref(desc), a["hidden"], a["weight"], a["draft_ids"], a["step_map"], a["num_ref"],
+        a["target_ids"], a["confidence"], a["draft_prob"], a["accept_len"], a["workspace"], a["ws"],
+        None)
+
+
+def test_lmhead_errors_and_workspace():
+    good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, hidden=128, dtype=binding.SIMSD_BF16)
+    d = LmheadDesc(**good)
+    # one 16-byte partial per (row, 256-entry vocabulary tile), 256-byte alignment, the
+    # merged partial of each row, alignment, then one float per draft slot
+    R, vt = 2 * 4, -(-1000 // 256)
+    merged_off = -(-(R * vt * 16) // 256) * 256
+    xdraft_off = -(-(merged_off + R * 16) // 256) * 256
+    assert binding.lmhead_workspace_size(d) == xdraft_off + 2 * 4 * 4
+    for k, v, st in [("batch", 0, 2), ("block_size", 65, 2), ("max_ref", 5, 2), ("vocab", 0, 2),
+                     ("hidden", 0, 2), ("hidden", 96, 2), ("dtype", binding.SIMSD_F32, 3)]:
+        bad = LmheadDesc(**dict(good, **{k: v}))
+        assert call_lmhead(bad) == st, (k, v)
+        assert binding.lib().simsd_verify_accept_lmhead_workspace_size(ctypes.byref(bad)) == 0
+    for k in ("hidden", "weight", "step_map", "num_ref", "target_ids", "accept_len", "draft_ids"):
+        assert call_lmhead(d, **{k: None}) == 1, k
+    assert call_lmhead(d, hidden=ctypes.c_void_p(0x10008)) == 4
+    assert call_lmhead(d, weight=ctypes.c_void_p(0x10004)) == 4
+    assert call_lmhead(d, workspace=None) == 5
+    assert call_lmhead(d, workspace=ctypes.c_void_p(0x10008)) == 4
+    assert call_lmhead(d, ws=binding.lmhead_workspace_size(d) - 1) == 5
 
 
 def d_cpr(desc, rows_per_seq):
