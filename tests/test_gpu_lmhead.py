@@ -68,3 +68,44 @@ def test_lmhead_parity(case):
     inp = generate(cfg, seed=seed, bad_draft_rate=0.2 if mode == "mixed" else 0.0)
     hidden, weight = generate_lmhead_side(inp, H)
     check_lmhead(inp, hidden, weight, run_lmhead(inp, hidden, weight))
+
+
+def test_lmhead_graph_replays_match_eager():
+    """The LM-head entry point captured in a HIP graph: every replay, with eager
+    work and synchronisation in between, reproduces the eager outputs bit for
+    bit (two row-count variants)."""
+    from paper_2606_02544_amd import binding
+    for b, B, L, V, H, seed in ((2, 8, 8, 3000, 256, 21), (12, 16, 16, 2051, 128, 22)):
+        cfg = VerifyConfig(0, "lmhead", "bf16", batch=b, num_q_heads=2, num_kv_heads=1,
+                           head_dim=64, prefix=4, block_size=B, max_ref=L, vocab=V, plant=0.6,
+                           step_mode="mixed")
+        inp = generate(cfg, seed=seed, bad_draft_rate=0.2)
+        hidden, weight = generate_lmhead_side(inp, H)
+        hd, wd = dev_tensor(hidden, "bf16"), dev_tensor(weight, "bf16")
+        ids, sm, nr = int_tensor(inp.draft_ids), int_tensor(inp.step_map), int_tensor(inp.num_ref)
+        eager = binding.verify_accept_lmhead(hd, wd, ids, sm, nr)
+        torch.cuda.synchronize()
+        outs = [torch.zeros_like(t) for t in eager]
+        s = torch.cuda.Stream()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            binding.verify_accept_lmhead(hd, wd, ids, sm, nr, target_ids=outs[0],
+                                         confidence=outs[1], draft_prob=outs[2],
+                                         accept_len=outs[3], stream=s)      # workspace exists
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=s):
+                binding.verify_accept_lmhead(hd, wd, ids, sm, nr, target_ids=outs[0],
+                                             confidence=outs[1], draft_prob=outs[2],
+                                             accept_len=outs[3], stream=s)
+        for rep in range(3):
+            for t in outs:
+                t.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            for x, y in zip(outs, eager):
+                assert torch.equal(x, y), (b, rep)
+            binding.verify_accept_lmhead(hd, wd, ids, sm, nr)    # eager work between replays
+            torch.cuda.synchronize()
+        check_lmhead(inp, hidden, weight, tuple(t.cpu().numpy() if t.dtype == torch.int32
+                                                else t.cpu().double().numpy() for t in outs))
