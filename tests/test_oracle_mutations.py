@@ -229,3 +229,44 @@ def test_rope_mutation_caught(monkeypatch, which):
                 monkeypatch.setattr(oattn, "prefix_kv", real_prefix)
         monkeypatch.setattr(oattn, "pair_attention", pair)
     assert not rope_pins_ok()
+
+
+import test_oracle_lmhead as tlm
+from oracle import lmhead as olm
+from oracle.widen import widen as _widen
+
+
+def lmhead_pins_ok():
+    try:
+        tlm.test_hand_example()
+        tlm.test_logits_against_element_sums()
+    except AssertionError:
+        return False
+    return True
+
+
+@pytest.mark.parametrize("which", ["dropped_last_term", "first_chunk_repeated", "slots_reversed",
+                                   "weight_rows_shifted"])
+def test_lmhead_mutation_caught(monkeypatch, which):
+    assert lmhead_pins_ok()
+    real = olm.lmhead_logits
+
+    def mutant(hidden, weight, dtype):
+        h = _widen(np.asarray(hidden), dtype)
+        w = _widen(np.asarray(weight), dtype)
+        if which == "dropped_last_term":
+            return h[..., :-1] @ w[:, :-1].T
+        if which == "first_chunk_repeated":            # chunk loop always reads chunk 0
+            step = 1 << 13
+            out = real(hidden, weight, dtype)
+            for v0 in range(step, w.shape[0], step):
+                n = min(step, w.shape[0] - v0)
+                out[..., v0:v0 + n] = h @ w[:n].T
+            return out
+        if which == "slots_reversed":
+            return h[:, ::-1] @ w.T
+        return h @ np.roll(w, 1, axis=0).T             # weight row v taken for token v + 1
+
+    monkeypatch.setattr(olm, "lmhead_logits", mutant)
+    monkeypatch.setattr(oracle, "lmhead_logits", mutant)
+    assert not lmhead_pins_ok()
