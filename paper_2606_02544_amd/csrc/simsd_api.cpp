@@ -118,9 +118,16 @@ extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const
   }
 }
 
+// Rows of the LM-head product, which pick the kernel variant and its vocabulary
+// tile (0 for a NULL descriptor, which the plan then rejects).
+static int lmhead_rows(const simsd_lmhead_desc* d) {
+  if (!d) return 0;
+  return static_cast<int>(std::min<int64_t>(int64_t{d->batch} * d->block_size, INT32_MAX));
+}
+
 extern "C" size_t simsd_verify_accept_lmhead_workspace_size(const simsd_lmhead_desc* desc) {
   LmheadPlan p;
-  if (plan_lmhead(desc, lmhead_vocab_tile(), lmhead_stage(), &p) != SIMSD_OK) return 0;
+  if (plan_lmhead(desc, lmhead_vocab_tile(lmhead_rows(desc)), lmhead_stage(), &p) != SIMSD_OK) return 0;
   return p.workspace;
 }
 
@@ -131,7 +138,7 @@ extern "C" simsd_status simsd_verify_accept_lmhead(
     void* workspace, size_t workspace_bytes, void* stream) {
   try {
     LmheadPlan p;
-    simsd_status st = plan_lmhead(desc, lmhead_vocab_tile(), lmhead_stage(), &p);
+    simsd_status st = plan_lmhead(desc, lmhead_vocab_tile(lmhead_rows(desc)), lmhead_stage(), &p);
     if (st != SIMSD_OK) return st;
     st = check_lmhead_args(desc, p, hidden, weight, draft_ids, step_map, num_ref, target_ids,
                            accept_len, workspace, workspace_bytes);

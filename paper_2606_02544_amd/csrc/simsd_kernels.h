@@ -83,7 +83,7 @@ hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p
 hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t stream);
 hipError_t launch_lmhead_merge(const LmheadArgs& a, hipStream_t st);
 hipError_t launch_finalize_lmhead(int batch, const AcceptArgs& a, hipStream_t stream);
-int lmhead_vocab_tile();   // vocabulary entries per scan work-group
+int lmhead_vocab_tile(int rows);   // vocabulary entries per scan work-group, by row count
 int lmhead_stage();        // reduction elements per stage (H must be a multiple)
 
 }  // namespace simsd

@@ -5,7 +5,7 @@
 // model's prediction there, the LM head applied to the slot's final hidden
 // state.  lmhead_scan_kernel computes those logits tile by tile on the matrix
 // cores -- logits^T[vocab, row] = W[vocab, :] . hidden[row, :]^T with
-// v_mfma_f32_32x32x16_bf16 -- and reduces each row over each 256-entry
+// v_mfma_f32_32x32x16_bf16 -- and reduces each row over each 128- or 256-entry
 // vocabulary tile to (max, lowest index reaching it, sum of exp(x - max)) in
 // the epilogue, the partial the logits scan writes, so the logits never reach
 // memory.  The tile that holds a row's drafted token also stores that logit
@@ -32,8 +32,9 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kNoIndex = 0x7fffffff;
 constexpr int NT = 512;                  // 8 waves: 4 vocabulary quarters x 2 row halves
-constexpr int TV = 256;                  // vocabulary entries per tile
-constexpr int VBW = TV / 128;            // 32-entry MFMA blocks per wave
+// Row-count thresholds of the variants (see launch_lmhead_scan).
+constexpr int kFewRows = 32;
+constexpr int kOneTileRows = 128;
 
 #define LM_LDS __attribute__((address_space(3)))
 
@@ -65,10 +66,12 @@ __device__ inline Best combine(Best a, Best b) {
   return r;
 }
 
-// TR rows per tile, KS reduction elements per stage, NBUF stages in the ring.
-template <int TR, int KS, int NBUF>
+// TR rows and TV vocabulary entries per tile, KS reduction elements per
+// stage, NBUF stages in the ring.
+template <int TR, int TV, int KS, int NBUF>
 __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   constexpr int RBW = TR / 64;             // 32-row MFMA blocks per wave
+  constexpr int VBW = TV / 128;            // 32-entry MFMA blocks per wave
   constexpr int CPR = KS / 8;              // 16-byte chunks per row per stage
   constexpr int ROWB = KS * 2;             // LDS bytes per row per stage
   constexpr int RPS = 16 / CPR;            // rows spanning the 64 banks
@@ -76,7 +79,7 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   constexpr int INSN = STAGEB / 1024;      // 1 KB direct loads per stage
   constexpr int PERW = INSN / (NT / 64);   // per wave
   constexpr int RPI = 64 / CPR;            // rows per direct load
-  static_assert(RBW >= 1 && TR % 64 == 0, "wave grid");
+  static_assert(RBW >= 1 && TR % 64 == 0 && VBW >= 1 && TV % 128 == 0, "wave grid");
   static_assert(KS % 16 == 0 && CPR <= 16, "stage width");
   static_assert(INSN % (NT / 64) == 0, "stage loads split evenly over the waves");
   static_assert(NBUF >= 2 && NBUF <= 5, "ring depth");
@@ -243,70 +246,89 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   }
 }
 
-// One wave per row merges the row's partials, one per vocabulary tile, so the
+// WPR waves per row merge the row's partials, one per vocabulary tile, so the
 // finalize kernel (one work-group per sequence) reads a single partial per row.
+// WPR = 8 (a work-group per row) for few rows, else one wave per row.
+template <int WPR>
 __global__ void __launch_bounds__(NT) lmhead_merge_kernel(LmheadArgs a) {
   constexpr int U = 8;                     // loads per lane in flight
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * (NT / 64) + (threadIdx.x >> 6);
-  if (row >= a.R) return;
-  const AcceptPartial* pr = a.part + static_cast<int64_t>(row) * a.vtiles;
+  constexpr int NW = NT / 64;
+  __shared__ Best s_w[NW];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row = blockIdx.x * (NW / WPR) + wave / WPR;
+  if (WPR == 1 && row >= a.R) return;
   Best r = {kNegInf, kNoIndex, 0.f};
-  for (int c0 = 0; c0 < a.vtiles; c0 += 64 * U) {
-    AcceptPartial v[U];
+  if (row < a.R) {
+    const AcceptPartial* pr = a.part + static_cast<int64_t>(row) * a.vtiles;
+    for (int c0 = 64 * (wave % WPR) + lane; c0 < a.vtiles; c0 += 64 * WPR * U) {
+      AcceptPartial v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (c0 + 64 * u + lane < a.vtiles) v[u] = pr[c0 + 64 * u + lane];
+      for (int u = 0; u < U; ++u)
+        if (c0 + 64 * WPR * u < a.vtiles) v[u] = pr[c0 + 64 * WPR * u];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (c0 + 64 * u + lane < a.vtiles) r = combine(r, Best{v[u].mx, v[u].ix, v[u].sm});
-  }
+      for (int u = 0; u < U; ++u)
+        if (c0 + 64 * WPR * u < a.vtiles) r = combine(r, Best{v[u].mx, v[u].ix, v[u].sm});
+    }
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    Best o;
-    o.mx = __shfl_xor(r.mx, off);
-    o.ix = __shfl_xor(r.ix, off);
-    o.sm = __shfl_xor(r.sm, off);
-    r = combine(r, o);
+    for (int off = 32; off >= 1; off >>= 1) {
+      Best o;
+      o.mx = __shfl_xor(r.mx, off);
+      o.ix = __shfl_xor(r.ix, off);
+      o.sm = __shfl_xor(r.sm, off);
+      r = combine(r, o);
+    }
   }
-  if (lane == 0) {
-    AcceptPartial m;
-    m.mx = r.mx;
-    m.ix = r.ix;
-    m.sm = r.sm;
-    m.pad = 0;
-    a.merged[row] = m;
+  if (WPR > 1) {                           // one row per work-group: combine its waves
+    if (lane == 0) s_w[wave] = r;
+    __syncthreads();
+    if (threadIdx.x != 0 || row >= a.R) return;
+    r = s_w[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) r = combine(r, s_w[w]);
+  } else if (lane != 0) {
+    return;
   }
+  AcceptPartial m;
+  m.mx = r.mx;
+  m.ix = r.ix;
+  m.sm = r.sm;
+  m.pad = 0;
+  a.merged[row] = m;
 }
 
 }  // namespace
 
 namespace {
-template <int TR, int KS, int NBUF>
+template <int TR, int TV, int KS, int NBUF>
 hipError_t launch_variant(const LmheadArgs& a, hipStream_t st) {
+  if (a.vtiles != (a.V + TV - 1) / TV) return hipErrorInvalidValue;   // plan and launch disagree
   const int ntiles = (a.R + TR - 1) / TR * a.vtiles;
-  hipLaunchKernelGGL((lmhead_scan_kernel<TR, KS, NBUF>), dim3((ntiles + 7) / 8 * 8), dim3(NT), 0,
-                     st, a);
+  hipLaunchKernelGGL((lmhead_scan_kernel<TR, TV, KS, NBUF>), dim3((ntiles + 7) / 8 * 8), dim3(NT),
+                     0, st, a);
   return hipGetLastError();
 }
 }  // namespace
 
 hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t st) {
-  // Few rows: the weight stream is all there is; 72 KB of LDS lets two
-  // work-groups share a CU.  Up to one row tile: 128-byte row segments, one
-  // work-group per CU.  More rows: 256-row tiles halve the weight re-reads and
-  // the LDS reads per MFMA.
-  if (a.R <= 32) return launch_variant<128, 32, 3>(a, st);
-  if (a.R <= 128) return launch_variant<128, 64, 3>(a, st);
-  return launch_variant<256, 64, 2>(a, st);
+  // Few rows: the weight stream is all there is; 128-entry vocabulary tiles
+  // (more, shorter work-groups) and 54 KB of LDS, two work-groups per CU.  Up
+  // to one row tile: 128-byte row segments, one work-group per CU.  More rows:
+  // 256-row tiles halve the weight re-reads and the LDS reads per MFMA.
+  if (a.R <= kFewRows) return launch_variant<128, 128, 32, 3>(a, st);
+  if (a.R <= kOneTileRows) return launch_variant<128, 256, 64, 3>(a, st);
+  return launch_variant<256, 256, 64, 2>(a, st);
 }
 
 hipError_t launch_lmhead_merge(const LmheadArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(lmhead_merge_kernel, dim3((a.R + NT / 64 - 1) / (NT / 64)), dim3(NT), 0, st, a);
+  if (a.R <= kFewRows)
+    hipLaunchKernelGGL(lmhead_merge_kernel<NT / 64>, dim3(a.R), dim3(NT), 0, st, a);
+  else
+    hipLaunchKernelGGL(lmhead_merge_kernel<1>, dim3((a.R + NT / 64 - 1) / (NT / 64)), dim3(NT), 0,
+                       st, a);
   return hipGetLastError();
 }
 
-int lmhead_vocab_tile() { return TV; }
+int lmhead_vocab_tile(int rows) { return rows <= kFewRows ? 128 : 256; }
 int lmhead_stage() { return 64; }   // the widest stage of the variants
 
 }  // namespace simsd

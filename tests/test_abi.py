@@ -235,12 +235,18 @@ def call_lmhead(desc, **over):
 def test_lmhead_errors_and_workspace():
     good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, hidden=128, dtype=binding.SIMSD_BF16)
     d = LmheadDesc(**good)
-    # one 16-byte partial per (row, 256-entry vocabulary tile), 256-byte alignment, the
-    # merged partial of each row, alignment, then one float per draft slot
-    R, vt = 2 * 4, -(-1000 // 256)
+    # one 16-byte partial per (row, vocabulary tile: 128 entries up to 32 rows, else 256),
+    # 256-byte alignment, the merged partial of each row, alignment, then one float per
+    # draft slot
+    R, vt = 2 * 4, -(-1000 // 128)
     merged_off = -(-(R * vt * 16) // 256) * 256
     xdraft_off = -(-(merged_off + R * 16) // 256) * 256
     assert binding.lmhead_workspace_size(d) == xdraft_off + 2 * 4 * 4
+    big = LmheadDesc(**dict(good, batch=16, block_size=32, max_ref=32, vocab=151936))
+    R, vt = 16 * 32, -(-151936 // 256)
+    merged_off = -(-(R * vt * 16) // 256) * 256
+    xdraft_off = -(-(merged_off + R * 16) // 256) * 256
+    assert binding.lmhead_workspace_size(big) == xdraft_off + 16 * 32 * 4
     for k, v, st in [("batch", 0, 2), ("block_size", 65, 2), ("max_ref", 5, 2), ("vocab", 0, 2),
                      ("hidden", 0, 2), ("hidden", 96, 2), ("dtype", binding.SIMSD_F32, 3)]:
         bad = LmheadDesc(**dict(good, **{k: v}))
