@@ -109,3 +109,19 @@ def test_lmhead_graph_replays_match_eager():
             torch.cuda.synchronize()
         check_lmhead(inp, hidden, weight, tuple(t.cpu().numpy() if t.dtype == torch.int32
                                                 else t.cpu().double().numpy() for t in outs))
+
+
+@pytest.mark.parametrize("gamma,committed,batch", [(0, 0, 3), (0, 3, 6), (3, 2, 6), (5, 0, 3)])
+def test_lmhead_steps_inside_a_block(gamma, committed, batch):
+    """Fewer drafts than block slots, committed slots, and the plain block step
+    (gamma = 0: no reference slots, draft_ids may be empty) on the LM-head path."""
+    cfg = VerifyConfig(0, "steps", "bf16", batch=batch, num_q_heads=2, num_kv_heads=1,
+                       head_dim=64, prefix=4, block_size=8, max_ref=gamma, vocab=3000,
+                       plant=0.6, committed=committed)
+    inp = generate(cfg, seed=90 + 7 * gamma + committed)
+    assert np.all(inp.num_ref == gamma)
+    hidden, weight = generate_lmhead_side(inp, 128)
+    got = run_lmhead(inp, hidden, weight)
+    check_lmhead(inp, hidden, weight, got)
+    if gamma == 0:
+        assert np.all(got[3] == 0)
