@@ -289,7 +289,19 @@ size_t simsd_verify_accept_lmhead_workspace_size(const simsd_lmhead_desc* desc);
  *   weight  [V, H] bf16, 16-byte aligned (a Linear layer's [out, in] layout)
  *   draft_ids, step_map, num_ref, target_ids, confidence, draft_prob,
  *   accept_len, workspace, workspace_bytes, stream   as for simsd_verify_accept
- * The workspace must hold simsd_verify_accept_lmhead_workspace_size() bytes.
+ *   (draft_ids may be NULL when max_ref == 0; confidence and draft_prob may be
+ *   NULL)
+ * The workspace must hold simsd_verify_accept_lmhead_workspace_size() bytes
+ * (0 for an invalid descriptor), 16-byte aligned, no initialisation needed; it
+ * is fully rewritten by each call, so calls on one stream may share it.  All
+ * buffers belong to the caller; the library allocates nothing and does not
+ * synchronise.  Three kernels are enqueued on the stream.  The fp32
+ * accumulation order is fixed for a given shape, so repeated calls give the
+ * same bits.
+ * Errors (nothing is enqueued): SIMSD_ERR_NULL_POINTER, SIMSD_ERR_BAD_SHAPE
+ * (descriptor out of range, H not a multiple of 64), SIMSD_ERR_UNSUPPORTED
+ * (dtype other than SIMSD_BF16), SIMSD_ERR_ALIGNMENT (hidden, weight or
+ * workspace), SIMSD_ERR_WORKSPACE; SIMSD_ERR_HIP if a launch fails.
  */
 simsd_status simsd_verify_accept_lmhead(const simsd_lmhead_desc* desc, const void* hidden,
                                         const void* weight, const int32_t* draft_ids,
