@@ -59,6 +59,19 @@ def workload_numbers(inp, sampled=False):
                 verified=int(np.sum(inp.num_ref)), scanned_rows=int(np.sum(inp.step_map >= 1)))
 
 
+def lmhead_roofline(flops, nbytes, call_ms):
+    """Roofline of the LM-head accept call (scan, merge and finalize kernels): bound by
+    MFMA when its intensity exceeds the bf16 ridge point, else by HBM."""
+    sec = call_ms * 1e-3
+    if flops / nbytes > BF16_MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+        a = flops / sec / 1e12
+        return {"bound": "mfma", "achieved": a, "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": a / BF16_MFMA_PEAK_TFLOPS}
+    a = nbytes / sec / 1e9
+    return {"bound": "hbm", "achieved": a, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": a / HBM_PEAK_GBS}
+
+
 def source_digest(paths):
     h = hashlib.sha256()
     for p in paths:
@@ -445,7 +458,8 @@ def main():
             "accept_us": acc_ms * 1e3,
             "accept_gbs": wl["accept_bytes"] / (acc_ms * 1e-3) / 1e9,
             **({"lmhead_tflops": wl["lmhead_flops"] / (acc_ms * 1e-3) / 1e12,
-                "lmhead_mfma_frac": wl["lmhead_flops"] / (acc_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS}
+                "lmhead_mfma_frac": wl["lmhead_flops"] / (acc_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+                "lmhead_roofline": lmhead_roofline(wl["lmhead_flops"], wl["accept_bytes"], acc_ms)}
                if args.lmhead else {}),
             "scanned_rows_per_s": wl["scanned_rows"] * K / elapsed,
             "attention_mfma_frac": wl["attn_flops"] / (attn_ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
