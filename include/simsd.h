@@ -55,6 +55,14 @@
  *    be NULL).  It holds per-chunk partial results between the kernels of one
  *    call; its contents need no initialisation and are meaningless afterwards.
  *    Two calls in flight at the same time need two workspaces.
+ *  - Grid sizes follow the compute-unit count of the device a call's stream
+ *    belongs to (queried once per device through the HIP device attributes
+ *    and cached; a compute-partitioned MI355X reports its partition's units).
+ *    The *_workspace_size() calls size for the current device (for an
+ *    MI355X's 256 units when no device is visible); a call on a device with
+ *    more units may need more and then returns SIMSD_ERR_WORKSPACE.  If the
+ *    device query fails, argument errors are still reported first, then
+ *    SIMSD_ERR_HIP.
  */
 #ifndef SIMSD_H
 #define SIMSD_H
@@ -76,7 +84,8 @@ typedef enum {
   SIMSD_ERR_ALIGNMENT = 4,        /* a pointer or stride is not 16-byte aligned       */
   SIMSD_ERR_WORKSPACE = 5,        /* workspace missing or smaller than required       */
   SIMSD_ERR_INVALID_STEP_MAP = 6, /* simsd_validate_step_map found a bad step map     */
-  SIMSD_ERR_HIP = 7               /* the HIP runtime reported an error on launch      */
+  SIMSD_ERR_HIP = 7               /* the HIP runtime reported an error (device query
+                                     or launch)                                       */
 } simsd_status;
 
 typedef enum {
@@ -102,8 +111,8 @@ typedef enum {
  * cache[p*cache_stride_seq + (t%page_size)*cache_stride_token +
  * h*cache_stride_head + i]  (cache_stride_seq is then the page stride).
  * The same layout and strides apply to k_cache and v_cache.  Strides are in
- * elements, non-negative, and must be multiples of 16 bytes.  The last index
- * (head_dim) is contiguous.
+ * elements, non-negative, at most 2^48, and must be multiples of 16 bytes.
+ * The last index (head_dim) is contiguous.
  */
 typedef struct {
   int32_t batch;              /* sequences, >= 1                                  */
@@ -317,7 +326,8 @@ simsd_status simsd_verify_accept_lmhead(const simsd_lmhead_desc* desc, const voi
 /* Checks host copies of step_map [batch, B] and num_ref [batch]: 0 <= gamma_b
  * <= L and every value 1..gamma_b exactly once per sequence.  Returns SIMSD_OK
  * or SIMSD_ERR_INVALID_STEP_MAP (SIMSD_ERR_NULL_POINTER / _BAD_SHAPE for bad
- * arguments), with the first offending sequence in simsd_last_error(). */
+ * arguments: batch >= 1, 1 <= B <= 64, 0 <= L <= B), with the first offending
+ * sequence in simsd_last_error(). */
 simsd_status simsd_validate_step_map(const int32_t* step_map_host, const int32_t* num_ref_host,
                                      int32_t batch, int32_t block_size, int32_t max_ref);
 

@@ -114,31 +114,108 @@ def _dtype_code(dt: torch.dtype) -> int:
     raise ValueError(f"unsupported dtype {dt}")
 
 
-def _stream(stream) -> ctypes.c_void_p:
+def _stream_of(stream, device: torch.device):
+    """The torch stream a call runs on: the given one, else the current stream
+    of the tensors' device."""
     if stream is None:
-        stream = torch.cuda.current_stream()
-    return ctypes.c_void_p(stream.cuda_stream)
+        stream = torch.cuda.current_stream(device)
+    return stream
+
+
+# ----------------------------------------------------------------------------
+# Argument checks.  The C library checks sizes, alignment and the workspace,
+# but it only sees pointers: shapes, dtypes, strides and devices of the
+# tensors are checked here, before any call, and raise ValueError.
+# ----------------------------------------------------------------------------
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _tensor(name: str, t, shape, dtype=None, device=None):
+    """t is a contiguous tensor of the given shape (None entries: any size),
+    dtype and device."""
+    _need(isinstance(t, torch.Tensor), f"{name} must be a torch.Tensor")
+    _need(t.dim() == len(shape), f"{name} must have {len(shape)} dimensions, got shape {tuple(t.shape)}")
+    for i, n in enumerate(shape):
+        _need(n is None or t.shape[i] == n,
+              f"{name} has shape {tuple(t.shape)}, expected {tuple('*' if x is None else x for x in shape)}")
+    if dtype is not None:
+        _need(t.dtype == dtype, f"{name} must be {dtype}, got {t.dtype}")
+    if device is not None:
+        _need(t.device == device, f"{name} is on {t.device}, expected {device}")
+    _need(t.is_contiguous(), f"{name} must be contiguous")
+
+
+def _int32(name, t, shape, device):
+    _tensor(name, t, shape, torch.int32, device)
+
+
+def _out(name, t, shape, dtype, device):
+    if t is not None:
+        _tensor(name, t, shape, dtype, device)
+
+
+def _check_cache(k_cache, v_cache, dtype, device, hkv, d, page_size, max_prefix_len,
+                 batch, block_table):
+    """k/v caches: same dtype as q, same shape and strides as each other, head
+    dim innermost with stride 1 (other strides are passed to the library)."""
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache)):
+        _need(isinstance(t, torch.Tensor) and t.dim() == 4,
+              f"{name} must be a 4-D tensor [seq or page, token, Hkv, d]")
+        _need(t.dtype == dtype, f"{name} must be {dtype} (the dtype of q), got {t.dtype}")
+        _need(t.device == device, f"{name} is on {t.device}, expected {device}")
+        _need(t.shape[2] == hkv and t.shape[3] == d,
+              f"{name} has shape {tuple(t.shape)}: need [*, *, {hkv}, {d}]")
+        _need(t.stride(3) == 1, f"{name} must have a unit stride over the head dimension")
+    _need(tuple(k_cache.shape) == tuple(v_cache.shape), "k_cache and v_cache shapes differ")
+    _need(k_cache.stride() == v_cache.stride(), "k_cache and v_cache strides differ")
+    if page_size > 0:
+        _need(k_cache.shape[1] == page_size,
+              f"paged cache: dimension 1 is {k_cache.shape[1]}, page_size is {page_size}")
+        _need(block_table is not None, "paged cache needs a block_table")
+        _int32("block_table", block_table, (batch, None), device)
+        _need(block_table.shape[1] * page_size >= max_prefix_len,
+              "block_table has too few pages per sequence for max_prefix_len")
+    else:
+        _need(k_cache.shape[0] == batch,
+              f"contiguous cache: dimension 0 is {k_cache.shape[0]}, batch is {batch}")
+        _need(k_cache.shape[1] >= max_prefix_len,
+              f"contiguous cache holds {k_cache.shape[1]} tokens, max_prefix_len is {max_prefix_len}")
 
 
 class _Workspaces:
-    """Scratch buffers for the workspace argument, one per (device, kind),
-    grown on demand.  The library needs no initialised contents."""
+    """Scratch buffers for the workspace argument, one per (device, stream,
+    kind), grown on demand.  The library needs no initialised contents.
+
+    Keyed by stream so that calls on different streams never share a buffer
+    (they could overlap on the device).  A buffer that is replaced by a larger
+    one is kept alive (in ``_retired``) rather than freed: a HIP graph captured
+    earlier may still launch kernels on it, and freed memory would be handed
+    to other tensors by the caching allocator.  ``clear()`` drops everything
+    and is only safe once no captured graph that used these buffers will be
+    replayed again."""
 
     def __init__(self):
         self._bufs = {}
+        self._retired = []
 
-    def get(self, device: torch.device, kind: str, nbytes: int) -> Optional[torch.Tensor]:
+    def get(self, device: torch.device, stream_handle: int, kind: str,
+            nbytes: int) -> Optional[torch.Tensor]:
         if nbytes == 0:
             return None
-        key = (str(device), kind)
+        key = (str(device), int(stream_handle), kind)
         buf = self._bufs.get(key)
         if buf is None or buf.numel() < nbytes:
+            if buf is not None:
+                self._retired.append(buf)
             buf = torch.empty(nbytes, dtype=torch.uint8, device=device)
             self._bufs[key] = buf
         return buf
 
     def clear(self):
         self._bufs.clear()
+        self._retired.clear()
 
 
 WORKSPACES = _Workspaces()
@@ -168,6 +245,43 @@ def accept_workspace_size(desc: AcceptDesc) -> int:
     return int(lib().simsd_verify_accept_workspace_size(ctypes.byref(desc)))
 
 
+def _workspace(workspace, device, stream, kind, nbytes):
+    """The caller's workspace (checked), or a cached one for this stream."""
+    if workspace is None:
+        return WORKSPACES.get(device, stream.cuda_stream, kind, nbytes)
+    _tensor("workspace", workspace, (None,), None, device)
+    return workspace
+
+
+def _nbytes(t: Optional[torch.Tensor]) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def check_attention_tensors(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens,
+                            step_map, num_ref, out, lse, *, block_size: int, max_ref: int,
+                            max_prefix_len: int, page_size: int):
+    """Shapes, dtypes, devices and layouts of the attention arguments."""
+    _need(isinstance(q, torch.Tensor) and q.dim() == 4, "q must be a 4-D tensor [batch, B+L, Hq, d]")
+    _need(q.dtype in (torch.bfloat16, torch.float32), f"q must be bfloat16 or float32, got {q.dtype}")
+    b, n_new, hq, d = q.shape
+    dev = q.device
+    _need(n_new == block_size + max_ref, f"q has {n_new} slots, block_size + max_ref is {block_size + max_ref}")
+    _tensor("q", q, (b, n_new, hq, d), q.dtype, dev)
+    _need(isinstance(k_new, torch.Tensor) and k_new.dim() == 4, "k_new must be a 4-D tensor")
+    hkv = k_new.shape[2]
+    _tensor("k_new", k_new, (b, n_new, hkv, d), q.dtype, dev)
+    _tensor("v_new", v_new, (b, n_new, hkv, d), q.dtype, dev)
+    if max_prefix_len > 0:
+        _check_cache(k_cache, v_cache, q.dtype, dev, hkv, d, page_size, max_prefix_len, b,
+                     block_table)
+    _int32("prefix_lens", prefix_lens, (b,), dev)
+    _int32("step_map", step_map, (b, block_size), dev)
+    _int32("num_ref", num_ref, (b,), dev)
+    _out("out", out, (b, n_new, hq, d), q.dtype, dev)
+    _out("lse", lse, (b, hq, n_new), torch.float32, dev)
+    return hkv
+
+
 def verify_attention(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens, step_map,
                      num_ref, *, block_size: int, max_ref: int, max_prefix_len: int,
                      page_size: int = 0, kv_chunk: int = 0, scale: float = 0.0,
@@ -175,26 +289,34 @@ def verify_attention(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      want_lse: bool = True, workspace: Optional[torch.Tensor] = None,
                      stream=None, desc: Optional[AttnDesc] = None):
-    """simsd_verify_attention on torch tensors.  Returns (out, lse)."""
+    """simsd_verify_attention on torch tensors.  Returns (out, lse).
+
+    Raises ValueError on tensors whose shape, dtype, device or layout does not
+    match (before anything is launched), SimsdError if the library rejects
+    the call."""
+    hkv = check_attention_tensors(q, k_new, v_new, k_cache, v_cache, block_table, prefix_lens,
+                                  step_map, num_ref, out, lse, block_size=block_size,
+                                  max_ref=max_ref, max_prefix_len=max_prefix_len,
+                                  page_size=page_size)
     if desc is None:
-        desc = attention_desc(q, k_cache, num_kv_heads=k_new.shape[2], block_size=block_size,
-                              max_ref=max_ref, max_prefix_len=max_prefix_len,
-                              page_size=page_size,
+        desc = attention_desc(q, k_cache if max_prefix_len > 0 else k_new, num_kv_heads=hkv,
+                              block_size=block_size, max_ref=max_ref,
+                              max_prefix_len=max_prefix_len, page_size=page_size,
                               max_pages_per_seq=(block_table.shape[1]
-                                                 if block_table is not None else 0),
+                                                 if block_table is not None and page_size > 0
+                                                 else 0),
                               kv_chunk=kv_chunk, scale=scale, rope_theta=rope_theta)
+    dev = q.device
     if out is None:
-        out = torch.empty_like(q)
+        out = torch.empty(q.shape, dtype=q.dtype, device=dev)
     if lse is None and want_lse:
-        lse = torch.empty((q.shape[0], q.shape[2], q.shape[1]), dtype=torch.float32,
-                          device=q.device)
-    if workspace is None:
-        workspace = WORKSPACES.get(q.device, "attn", attention_workspace_size(desc))
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        lse = torch.empty((q.shape[0], q.shape[2], q.shape[1]), dtype=torch.float32, device=dev)
+    st = _stream_of(stream, dev)
+    workspace = _workspace(workspace, dev, st, "attn", attention_workspace_size(desc))
     _check(lib().simsd_verify_attention(
         ctypes.byref(desc), _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(k_cache), _ptr(v_cache),
         _ptr(block_table), _ptr(prefix_lens), _ptr(step_map), _ptr(num_ref), _ptr(out),
-        _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream)))
+        _ptr(lse), _ptr(workspace), _nbytes(workspace), ctypes.c_void_p(st.cuda_stream)))
     return out, lse
 
 
@@ -204,16 +326,33 @@ def accept_desc(logits: torch.Tensor, max_ref: int, chunks_per_row: int = 0) -> 
                       chunks_per_row=chunks_per_row, logits_dtype=_dtype_code(logits.dtype))
 
 
+def _check_accept_inputs(logits, draft_ids, step_map, num_ref):
+    _need(isinstance(logits, torch.Tensor) and logits.dim() == 3, "logits must be a 3-D tensor [batch, B, V]")
+    _need(logits.dtype in (torch.bfloat16, torch.float32),
+          f"logits must be bfloat16 or float32, got {logits.dtype}")
+    b, B, V = logits.shape
+    dev = logits.device
+    _tensor("logits", logits, (b, B, V), logits.dtype, dev)
+    _need(isinstance(draft_ids, torch.Tensor) and draft_ids.dim() == 2,
+          "draft_ids must be a 2-D tensor [batch, L]")
+    _int32("draft_ids", draft_ids, (b, None), dev)
+    _int32("step_map", step_map, (b, B), dev)
+    _int32("num_ref", num_ref, (b,), dev)
+    return b, B, V, draft_ids.shape[1], dev
+
+
 def verify_accept(logits, draft_ids, step_map, num_ref, *, chunks_per_row: int = 0,
                   target_ids=None, confidence=None, draft_prob=None, accept_len=None,
                   workspace=None, stream=None, desc: Optional[AcceptDesc] = None):
     """simsd_verify_accept on torch tensors.
     Returns (target_ids, confidence, draft_prob, accept_len)."""
-    b, B, V = logits.shape
-    L = draft_ids.shape[1]
+    b, B, V, L, dev = _check_accept_inputs(logits, draft_ids, step_map, num_ref)
+    _out("target_ids", target_ids, (b, B), torch.int32, dev)
+    _out("confidence", confidence, (b, B), torch.float32, dev)
+    _out("draft_prob", draft_prob, (b, L), torch.float32, dev)
+    _out("accept_len", accept_len, (b,), torch.int32, dev)
     if desc is None:
         desc = accept_desc(logits, L, chunks_per_row)
-    dev = logits.device
     if target_ids is None:
         target_ids = torch.empty((b, B), dtype=torch.int32, device=dev)
     if confidence is None:
@@ -222,13 +361,12 @@ def verify_accept(logits, draft_ids, step_map, num_ref, *, chunks_per_row: int =
         draft_prob = torch.empty((b, L), dtype=torch.float32, device=dev)
     if accept_len is None:
         accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = WORKSPACES.get(dev, "accept", accept_workspace_size(desc))
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _stream_of(stream, dev)
+    workspace = _workspace(workspace, dev, st, "accept", accept_workspace_size(desc))
     _check(lib().simsd_verify_accept(
         ctypes.byref(desc), _ptr(logits), _ptr(draft_ids), _ptr(step_map), _ptr(num_ref),
         _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
-        _ptr(workspace), ws_bytes, _stream(stream)))
+        _ptr(workspace), _nbytes(workspace), ctypes.c_void_p(st.cuda_stream)))
     return target_ids, confidence, draft_prob, accept_len
 
 
@@ -242,11 +380,15 @@ def verify_accept_sampled(logits, draft_logits, draft_ids, step_map, num_ref, un
                           stream=None, desc: Optional[AcceptDesc] = None):
     """simsd_verify_accept_sampled on torch tensors.
     Returns (p_target, p_draft, accept_len, correction)."""
-    b, B, V = logits.shape
-    L = draft_ids.shape[1]
+    b, B, V, L, dev = _check_accept_inputs(logits, draft_ids, step_map, num_ref)
+    _tensor("draft_logits", draft_logits, (b, L, V), logits.dtype, dev)
+    _tensor("uniforms", uniforms, (b, L + 1), torch.float32, dev)
+    _out("p_target", p_target, (b, L), torch.float32, dev)
+    _out("p_draft", p_draft, (b, L), torch.float32, dev)
+    _out("accept_len", accept_len, (b,), torch.int32, dev)
+    _out("correction", correction, (b,), torch.int32, dev)
     if desc is None:
         desc = accept_desc(logits, L, chunks_per_row)
-    dev = logits.device
     if p_target is None:
         p_target = torch.empty((b, L), dtype=torch.float32, device=dev)
     if p_draft is None:
@@ -255,14 +397,14 @@ def verify_accept_sampled(logits, draft_logits, draft_ids, step_map, num_ref, un
         accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
     if correction is None:
         correction = torch.empty((b,), dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = WORKSPACES.get(dev, "accept_sampled", accept_sampled_workspace_size(desc))
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _stream_of(stream, dev)
+    workspace = _workspace(workspace, dev, st, "accept_sampled",
+                           accept_sampled_workspace_size(desc))
     _check(lib().simsd_verify_accept_sampled(
         ctypes.byref(desc), ctypes.c_float(temperature), _ptr(logits), _ptr(draft_logits),
         _ptr(draft_ids), _ptr(step_map), _ptr(num_ref), _ptr(uniforms), _ptr(p_target),
-        _ptr(p_draft), _ptr(accept_len), _ptr(correction), _ptr(workspace), ws_bytes,
-        _stream(stream)))
+        _ptr(p_draft), _ptr(accept_len), _ptr(correction), _ptr(workspace),
+        _nbytes(workspace), ctypes.c_void_p(st.cuda_stream)))
     return p_target, p_draft, accept_len, correction
 
 
@@ -281,11 +423,26 @@ def verify_accept_lmhead(hidden, weight, draft_ids, step_map, num_ref, *, target
                          stream=None, desc: Optional[LmheadDesc] = None):
     """simsd_verify_accept_lmhead on torch tensors (hidden [b, B, H], weight [V, H]).
     Returns (target_ids, confidence, draft_prob, accept_len)."""
+    _need(isinstance(hidden, torch.Tensor) and hidden.dim() == 3,
+          "hidden must be a 3-D tensor [batch, B, H]")
     b, B, H = hidden.shape
+    dev = hidden.device
+    _tensor("hidden", hidden, (b, B, H), torch.bfloat16, dev)
+    _need(isinstance(weight, torch.Tensor) and weight.dim() == 2, "weight must be a 2-D tensor [V, H]")
+    _tensor("weight", weight, (None, H), torch.bfloat16, dev)
+    V = weight.shape[0]
+    _need(isinstance(draft_ids, torch.Tensor) and draft_ids.dim() == 2,
+          "draft_ids must be a 2-D tensor [batch, L]")
+    _int32("draft_ids", draft_ids, (b, None), dev)
+    _int32("step_map", step_map, (b, B), dev)
+    _int32("num_ref", num_ref, (b,), dev)
     L = draft_ids.shape[1]
+    _out("target_ids", target_ids, (b, B), torch.int32, dev)
+    _out("confidence", confidence, (b, B), torch.float32, dev)
+    _out("draft_prob", draft_prob, (b, L), torch.float32, dev)
+    _out("accept_len", accept_len, (b,), torch.int32, dev)
     if desc is None:
         desc = lmhead_desc(hidden, weight, L)
-    dev = hidden.device
     if target_ids is None:
         target_ids = torch.empty((b, B), dtype=torch.int32, device=dev)
     if confidence is None:
@@ -294,13 +451,12 @@ def verify_accept_lmhead(hidden, weight, draft_ids, step_map, num_ref, *, target
         draft_prob = torch.empty((b, L), dtype=torch.float32, device=dev)
     if accept_len is None:
         accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
-    if workspace is None:
-        workspace = WORKSPACES.get(dev, "lmhead", lmhead_workspace_size(desc))
-    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = _stream_of(stream, dev)
+    workspace = _workspace(workspace, dev, st, "lmhead", lmhead_workspace_size(desc))
     _check(lib().simsd_verify_accept_lmhead(
         ctypes.byref(desc), _ptr(hidden), _ptr(weight), _ptr(draft_ids), _ptr(step_map),
         _ptr(num_ref), _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
-        _ptr(workspace), ws_bytes, _stream(stream)))
+        _ptr(workspace), _nbytes(workspace), ctypes.c_void_p(st.cuda_stream)))
     return target_ids, confidence, draft_prob, accept_len
 
 

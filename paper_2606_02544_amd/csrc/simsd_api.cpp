@@ -1,6 +1,7 @@
 // extern "C" compute entry points: check, plan, fill the argument block, launch.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <string>
 
 #include "simsd.h"
@@ -16,19 +17,85 @@ static simsd_status hip_fail(hipError_t e, const char* what) {
   return SIMSD_ERR_HIP;
 }
 
+// Compute units of device `dev`, queried once per device and cached (an
+// attribute query: no allocation, no synchronisation).  A compute-partitioned
+// MI355X reports the units of its partition.
+static constexpr int kMaxDevices = 64;
+static std::atomic<int> g_device_cus[kMaxDevices];
+
+static hipError_t device_cus(int dev, int* cus) {
+  if (dev >= 0 && dev < kMaxDevices) {
+    const int v = g_device_cus[dev].load(std::memory_order_relaxed);
+    if (v > 0) {
+      *cus = v;
+      return hipSuccess;
+    }
+  }
+  int n = 0;
+  const hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  if (n < 1) return hipErrorInvalidDevice;
+  if (dev >= 0 && dev < kMaxDevices) g_device_cus[dev].store(n, std::memory_order_relaxed);
+  *cus = n;
+  return hipSuccess;
+}
+
+// Compute units of the device a stream belongs to (the current device for
+// the null stream).  When the query fails, *cus is the nominal count of an
+// MI355X, so that argument errors are still reported first; the caller
+// returns the query's error after validation.
+static constexpr int kNominalCUs = 256;
+
+static hipError_t stream_cus(void* stream, int* cus) {
+  hipDevice_t dev = 0;
+  hipError_t e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &dev);
+  if (e == hipSuccess) e = device_cus(dev, cus);
+  if (e != hipSuccess) *cus = kNominalCUs;
+  return e;
+}
+
+// Compute units of the current device (workspace-size queries have no
+// stream); the nominal count when no device is visible.
+static int current_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || device_cus(dev, &cus) != hipSuccess) return kNominalCUs;
+  return cus;
+}
+
+extern "C" size_t simsd_verify_attention_workspace_size(const simsd_attn_desc* desc) {
+  AttnPlan p;
+  if (plan_attention(desc, current_cus(), &p) != SIMSD_OK) return 0;
+  return p.workspace;
+}
+
+extern "C" size_t simsd_verify_accept_workspace_size(const simsd_accept_desc* desc) {
+  AcceptPlan p;
+  if (plan_accept(desc, current_cus(), &p) != SIMSD_OK) return 0;
+  return p.workspace;
+}
+
+extern "C" size_t simsd_verify_accept_sampled_workspace_size(const simsd_accept_desc* desc) {
+  AcceptPlan p;
+  if (plan_accept(desc, current_cus(), &p, true) != SIMSD_OK) return 0;
+  return p.workspace;
+}
+
 extern "C" simsd_status simsd_verify_attention(
     const simsd_attn_desc* desc, const void* q, const void* k_new, const void* v_new,
     const void* k_cache, const void* v_cache, const int32_t* block_table,
     const int32_t* prefix_lens, const int32_t* step_map, const int32_t* num_ref, void* out,
     float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   try {
+    int cus = 0;
+    const hipError_t qe = stream_cus(stream, &cus);
     AttnPlan p;
-    simsd_status st = plan_attention(desc, &p);
+    simsd_status st = plan_attention(desc, cus, &p);
     if (st != SIMSD_OK) return st;
     st = check_attention_args(desc, p, q, k_new, v_new, k_cache, v_cache, block_table,
                               prefix_lens, step_map, num_ref, out, lse, workspace,
                               workspace_bytes);
     if (st != SIMSD_OK) return st;
+    if (qe != hipSuccess) return hip_fail(qe, "simsd_verify_attention: device query");
     AttnArgs a{};
     a.q = q;
     a.k_new = k_new;
@@ -85,12 +152,15 @@ extern "C" simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const
                                             int32_t* accept_len, void* workspace,
                                             size_t workspace_bytes, void* stream) {
   try {
+    int cus = 0;
+    const hipError_t qe = stream_cus(stream, &cus);
     AcceptPlan p;
-    simsd_status st = plan_accept(desc, &p);
+    simsd_status st = plan_accept(desc, cus, &p);
     if (st != SIMSD_OK) return st;
     st = check_accept_args(desc, p, logits, draft_ids, step_map, num_ref, target_ids,
                            confidence, draft_prob, accept_len, workspace, workspace_bytes);
     if (st != SIMSD_OK) return st;
+    if (qe != hipSuccess) return hip_fail(qe, "simsd_verify_accept: device query");
     AcceptArgs a{};
     a.logits = logits;
     a.draft_ids = draft_ids;
@@ -194,13 +264,16 @@ extern "C" simsd_status simsd_verify_accept_sampled(
     const float* uniforms, float* p_target, float* p_draft, int32_t* accept_len,
     int32_t* correction, void* workspace, size_t workspace_bytes, void* stream) {
   try {
+    int cus = 0;
+    const hipError_t qe = stream_cus(stream, &cus);
     AcceptPlan p;
-    simsd_status st = plan_accept(desc, &p, true);
+    simsd_status st = plan_accept(desc, cus, &p, true);
     if (st != SIMSD_OK) return st;
     st = check_accept_sampled_args(desc, p, temperature, logits, draft_logits, draft_ids, step_map,
                                    num_ref, uniforms, accept_len, correction, workspace,
                                    workspace_bytes);
     if (st != SIMSD_OK) return st;
+    if (qe != hipSuccess) return hip_fail(qe, "simsd_verify_accept_sampled: device query");
     AcceptArgs a{};
     a.logits = logits;
     a.draft_logits = draft_logits;

@@ -5,8 +5,8 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstring>
 #include <string>
-#include <vector>
 
 namespace simsd {
 
@@ -25,9 +25,24 @@ static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 static int elem_bytes(simsd_dtype t) { return t == SIMSD_F32 ? 4 : 2; }
 
-simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
+// A dtype field as the integer a C caller stored there.  Reading the enum
+// itself would be undefined for a value outside the enumeration, which the
+// ABI must reject rather than trust.
+static_assert(sizeof(simsd_dtype) == sizeof(int), "simsd_dtype is int-sized");
+static int dtype_code(const simsd_dtype& field) {
+  int v;
+  std::memcpy(&v, &field, sizeof v);
+  return v;
+}
+static bool known_dtype(const simsd_dtype& field) {
+  const int v = dtype_code(field);
+  return v == SIMSD_F32 || v == SIMSD_BF16;
+}
+
+simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p) {
   if (!d || !p) return fail(SIMSD_ERR_NULL_POINTER, "attention: descriptor is NULL");
-  if (d->dtype != SIMSD_F32 && d->dtype != SIMSD_BF16)
+  if (cus < 1) return fail(SIMSD_ERR_HIP, "attention: the device reports no compute units");
+  if (!known_dtype(d->dtype))
     return fail(SIMSD_ERR_UNSUPPORTED, "attention: dtype must be SIMSD_F32 or SIMSD_BF16");
   if (d->batch < 1 || d->batch > 65535)
     return fail(SIMSD_ERR_BAD_SHAPE, "attention: batch must be in [1, 65535]");
@@ -39,7 +54,7 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   if (d->head_dim != 64 && d->head_dim != 128)
     return fail(SIMSD_ERR_UNSUPPORTED, "attention: head_dim must be 64 or 128");
   if (d->block_size < 1 || d->max_ref < 0 || d->max_ref > d->block_size ||
-      d->block_size + d->max_ref > kMaxNew)
+      int64_t{d->block_size} + d->max_ref > kMaxNew)
     return fail(SIMSD_ERR_BAD_SHAPE,
                 "attention: need block_size >= 1, 0 <= max_ref <= block_size, "
                 "block_size + max_ref <= 64");
@@ -55,8 +70,11 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   const int64_t strides[3] = {d->cache_stride_seq, d->cache_stride_token, d->cache_stride_head};
   for (int64_t s : strides) {
     if (s < 0) return fail(SIMSD_ERR_BAD_SHAPE, "attention: negative cache stride");
-    if ((s * eb) % 16 != 0)
+    // s * eb a multiple of 16 bytes, tested without forming the product
+    if (s % (16 / eb) != 0)
       return fail(SIMSD_ERR_ALIGNMENT, "attention: cache strides must be multiples of 16 bytes");
+    if (s > (int64_t{1} << 48))
+      return fail(SIMSD_ERR_BAD_SHAPE, "attention: cache stride beyond 2^48 elements");
   }
   if (!(std::isfinite(d->scale) && d->scale >= 0.f))
     return fail(SIMSD_ERR_BAD_SHAPE, "attention: scale must be finite and >= 0");
@@ -90,7 +108,7 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
   } else {
     // Split the longest prefix so that about as many work-groups exist as the
     // chip holds at once: one 8-wave group or two smaller groups per CU.
-    const int64_t target = r.waves >= 8 ? kCUs : 2 * kCUs;
+    const int64_t target = r.waves >= 8 ? cus : 2 * int64_t{cus};
     int64_t c = ceil_div(static_cast<int64_t>(d->max_prefix_len) * r.pairs, target);
     c = ceil_div(c, kTile) * kTile;
     if (c < kMinAutoChunk) c = kMinAutoChunk;
@@ -115,7 +133,7 @@ simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p) {
                 "attention: kv_chunk -1 (stream) needs bf16, at most 128 packed rows "
                 "(Hq/Hkv * (B + L)) and batch <= 256");
   if (can_stream && d->kv_chunk <= 0) {
-    const int64_t groups = r.waves >= 8 ? kCUs : 2 * kCUs;
+    const int64_t groups = r.waves >= 8 ? cus : 2 * int64_t{cus};
     const int64_t tiles = r.pairs * (ceil_div(d->max_prefix_len, kTile) + 1);
     if (d->kv_chunk == kStreamChunk || (tiles >= 8 * groups && r.pairs * r.splits > groups)) {
       r.stream = true;
@@ -161,9 +179,10 @@ simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, c
   return SIMSD_OK;
 }
 
-simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled) {
+simsd_status plan_accept(const simsd_accept_desc* d, int cus, AcceptPlan* p, bool sampled) {
   if (!d || !p) return fail(SIMSD_ERR_NULL_POINTER, "accept: descriptor is NULL");
-  if (d->logits_dtype != SIMSD_F32 && d->logits_dtype != SIMSD_BF16)
+  if (cus < 1) return fail(SIMSD_ERR_HIP, "accept: the device reports no compute units");
+  if (!known_dtype(d->logits_dtype))
     return fail(SIMSD_ERR_UNSUPPORTED, "accept: logits_dtype must be SIMSD_F32 or SIMSD_BF16");
   if (d->batch < 1 || d->batch > 65535)
     return fail(SIMSD_ERR_BAD_SHAPE, "accept: batch must be in [1, 65535]");
@@ -182,7 +201,7 @@ simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled
   const int64_t rows = static_cast<int64_t>(d->batch) * r.rows;
   int64_t cpr = d->chunks_per_row;
   if (cpr == 0) {
-    cpr = ceil_div(kAcceptTarget, rows);
+    cpr = ceil_div(int64_t{kAcceptPerCU} * cus, rows);
     const int64_t most = std::max<int64_t>(1, r.nvec / kAcceptThreads);
     if (cpr > most) cpr = most;
   }
@@ -192,8 +211,9 @@ simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled
   r.chunk_vecs = ceil_div(r.nvec, r.cpr);
   r.workspace = static_cast<size_t>(rows) * r.cpr * sizeof(AcceptPartial);
   if (sampled) {
-    // About kAcceptTarget draw work-groups, each at least one vector per thread.
-    int64_t g = ceil_div(kAcceptTarget, d->batch);
+    // About kAcceptPerCU draw work-groups per compute unit, each at least one
+    // vector per thread.
+    int64_t g = ceil_div(int64_t{kAcceptPerCU} * cus, d->batch);
     const int64_t most = std::max<int64_t>(1, r.nvec / kAcceptThreads);
     g = std::min<int64_t>(std::min<int64_t>(g, most), kAcceptThreads);
     r.draw_chunks = static_cast<int>(std::max<int64_t>(g, 1));
@@ -229,7 +249,8 @@ simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
 
 simsd_status plan_lmhead(const simsd_lmhead_desc* d, int vocab_tile, int stage, LmheadPlan* p) {
   if (!d || !p) return fail(SIMSD_ERR_NULL_POINTER, "lmhead: descriptor is NULL");
-  if (d->dtype != SIMSD_BF16) return fail(SIMSD_ERR_UNSUPPORTED, "lmhead: dtype must be SIMSD_BF16");
+  if (dtype_code(d->dtype) != SIMSD_BF16)
+    return fail(SIMSD_ERR_UNSUPPORTED, "lmhead: dtype must be SIMSD_BF16");
   if (d->batch < 1 || d->batch > 65535)
     return fail(SIMSD_ERR_BAD_SHAPE, "lmhead: batch must be in [1, 65535]");
   if (d->block_size < 1 || d->block_size > kMaxNew)
@@ -307,31 +328,14 @@ simsd_status check_accept_sampled_args(const simsd_accept_desc* d, const AcceptP
 
 using namespace simsd;
 
-extern "C" size_t simsd_verify_attention_workspace_size(const simsd_attn_desc* desc) {
-  AttnPlan p;
-  if (plan_attention(desc, &p) != SIMSD_OK) return 0;
-  return p.workspace;
-}
-
-extern "C" size_t simsd_verify_accept_workspace_size(const simsd_accept_desc* desc) {
-  AcceptPlan p;
-  if (plan_accept(desc, &p) != SIMSD_OK) return 0;
-  return p.workspace;
-}
-
-extern "C" size_t simsd_verify_accept_sampled_workspace_size(const simsd_accept_desc* desc) {
-  AcceptPlan p;
-  if (plan_accept(desc, &p, true) != SIMSD_OK) return 0;
-  return p.workspace;
-}
-
 extern "C" simsd_status simsd_validate_step_map(const int32_t* step_map, const int32_t* num_ref,
                                                 int32_t batch, int32_t block_size,
                                                 int32_t max_ref) {
   if (!step_map || !num_ref) return fail(SIMSD_ERR_NULL_POINTER, "validate_step_map: NULL array");
-  if (batch < 1 || block_size < 1 || max_ref < 0 || max_ref > block_size)
-    return fail(SIMSD_ERR_BAD_SHAPE, "validate_step_map: bad batch/block_size/max_ref");
-  std::vector<int> seen(static_cast<size_t>(block_size) + 1);
+  if (batch < 1 || block_size < 1 || block_size > kMaxNew || max_ref < 0 || max_ref > block_size)
+    return fail(SIMSD_ERR_BAD_SHAPE,
+                "validate_step_map: need batch >= 1, 1 <= block_size <= 64, 0 <= max_ref <= block_size");
+  int seen[kMaxNew + 1];
   for (int32_t b = 0; b < batch; ++b) {
     const int32_t gamma = num_ref[b];
     if (gamma < 0 || gamma > max_ref) {
@@ -339,7 +343,7 @@ extern "C" simsd_status simsd_validate_step_map(const int32_t* step_map, const i
       std::snprintf(buf, sizeof buf, "sequence %d: num_ref %d outside [0, %d]", b, gamma, max_ref);
       return fail(SIMSD_ERR_INVALID_STEP_MAP, buf);
     }
-    std::fill(seen.begin(), seen.end(), 0);
+    std::fill(seen, seen + block_size + 1, 0);
     for (int32_t k = 0; k < block_size; ++k) {
       const int32_t s = step_map[static_cast<int64_t>(b) * block_size + k];
       if (s >= 1 && s <= gamma) ++seen[s];

@@ -13,13 +13,12 @@ namespace simsd {
 constexpr int kTile = 64;            // keys per attention tile
 constexpr int kMaxNew = 64;          // B + L limit (one 64-bit visibility word per row)
 constexpr int kMaxGroup = 16;        // Hq / Hkv limit
-constexpr int kCUs = 256;            // compute units of an MI355X
 constexpr int kStreamChunk = -1;    // kv_chunk value that asks for the stream decomposition
 constexpr int kMaxStreamBatch = 256;  // stream decomposition: largest batch
 constexpr int kMinAutoChunk = 64;   // shortest automatic prefix chunk (keys)
 constexpr int kMaxAutoChunk = 8192;  // longest automatic prefix chunk (keys)
 constexpr int kAcceptThreads = 256;  // threads of the vocabulary-scan work-group
-constexpr int kAcceptTarget = 512;   // scan work-groups the chunk heuristic aims for
+constexpr int kAcceptPerCU = 2;     // scan work-groups per compute unit the chunk heuristic aims for
 
 struct AttnPlan {
   int group = 0;        // Hq / Hkv
@@ -86,7 +85,9 @@ struct DrawPartial {
 
 void set_error(const std::string& msg);
 
-simsd_status plan_attention(const simsd_attn_desc* d, AttnPlan* p);
+// `cus`: compute units of the device the call runs on (it sizes the grids and
+// the stream decomposition's workspace); must be >= 1.
+simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p);
 simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, const void* q,
                                   const void* k_new, const void* v_new, const void* k_cache,
                                   const void* v_cache, const int32_t* block_table,
@@ -95,7 +96,7 @@ simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, c
                                   const void* workspace, size_t workspace_bytes);
 
 // sampled: the stochastic entry point, whose scan also covers the L draft rows.
-simsd_status plan_accept(const simsd_accept_desc* d, AcceptPlan* p, bool sampled = false);
+simsd_status plan_accept(const simsd_accept_desc* d, int cus, AcceptPlan* p, bool sampled = false);
 simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const void* logits, const int32_t* draft_ids,
                                const int32_t* step_map, const int32_t* num_ref,

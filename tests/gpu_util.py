@@ -93,3 +93,21 @@ def check_accept(got, ref):
 def oracle_accept(inp):
     return oracle.verify_accept(inp.logits, inp.draft_ids, inp.step_map, inp.num_ref,
                                 inp.cfg.dtype)
+
+
+def walk_accept(target_ids, draft_ids, step_map, num_ref):
+    """Accepted-prefix length from a given set of target ids (Sec. 3.2, the
+    longest accepted prefix of eq. 2 at temperature 0): for each sequence, the
+    number of leading drafts r = 1..gamma whose token equals the target id of
+    the block slot k_r with step_map = r.  Used where several target ids are
+    valid (near-ties of fp32-accumulated logits), so that accept_len is always
+    checked against the ids the GPU actually produced."""
+    b = len(num_ref)
+    out = np.zeros((b,), np.int32)
+    for s in range(b):
+        for r in range(int(num_ref[s])):
+            k = int(np.flatnonzero(step_map[s] == r + 1)[0])
+            if int(target_ids[s, k]) != int(draft_ids[s, r]):
+                break
+            out[s] += 1
+    return out

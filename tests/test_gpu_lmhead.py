@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import dev_tensor, int_tensor
+from gpu_util import dev_tensor, int_tensor, walk_accept
 from synth import VerifyConfig, config_by_id, generate, generate_lmhead_side
 
 pytestmark = pytest.mark.gpu
@@ -38,6 +38,9 @@ def check_lmhead(inp, hidden, weight, got):
                 (s, k, t[s, k], rt[s, k])
             near += 1
     assert np.all(t[~scanned] == -1)
+    # The accepted length always follows the ids the GPU produced; where none
+    # differs from the oracle's it is also the oracle's length.
+    np.testing.assert_array_equal(a, walk_accept(t, inp.draft_ids, inp.step_map, inp.num_ref))
     if near == 0:
         np.testing.assert_array_equal(a, ra)
     np.testing.assert_allclose(c, rc, rtol=1e-4, atol=1e-30)
@@ -125,3 +128,16 @@ def test_lmhead_steps_inside_a_block(gamma, committed, batch):
     check_lmhead(inp, hidden, weight, got)
     if gamma == 0:
         assert np.all(got[3] == 0)
+
+
+@pytest.mark.parametrize("batch,B", [(8, 16), (16, 32)])
+def test_lmhead_8b_head(batch, B):
+    """The SDAR-8B-shaped head (H = 4096, V = 151936) at the row counts of the
+    8B layer (128 rows: 64-wide stages) and the long-context step (512 rows:
+    256-row tiles), gamma = B as in the workloads."""
+    cfg = VerifyConfig(0, "lmhead8b", "bf16", batch=batch, num_q_heads=2, num_kv_heads=1,
+                       head_dim=64, prefix=4, block_size=B, max_ref=B, vocab=151936,
+                       plant=0.6, step_mode="full")
+    inp = generate(cfg, seed=100 + B)
+    hidden, weight = generate_lmhead_side(inp, 4096)
+    check_lmhead(inp, hidden, weight, run_lmhead(inp, hidden, weight))
