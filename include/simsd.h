@@ -230,6 +230,37 @@ simsd_status simsd_verify_accept(const simsd_accept_desc* desc, const void* logi
                                  void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the greedy
+ * verification of simsd_verify_accept with no workspace argument.  The scan
+ * partials go to a fixed device array of SIMSD_NOALLOC_SCRATCH_BYTES inside the
+ * library; each GPU the library runs on holds its own copy of it until the
+ * process ends.
+ *
+ *   desc, logits, draft_ids, step_map, num_ref, target_ids, confidence,
+ *   draft_prob, accept_len, stream     exactly as for simsd_verify_accept,
+ *                                      and the outputs are the same bits
+ *
+ * Nothing is allocated, freed or synchronised by the call; its first call on a
+ * device looks up that device's copy of the array (making the device current
+ * for the lookup and restoring the previous one).  Shapes whose partials need
+ * more than SIMSD_NOALLOC_SCRATCH_BYTES (16 bytes per scanned row and
+ * vocabulary chunk, the size simsd_verify_accept_workspace_size reports)
+ * return SIMSD_ERR_WORKSPACE with nothing enqueued: use simsd_verify_accept
+ * with a workspace for those.  All calls on one GPU share its array, which
+ * keeps the last call's contents (every entry is written before it is read, so
+ * nothing needs clearing): calls that overlap on one GPU, on any streams, race
+ * and must be serialised by the caller.  Other errors as simsd_verify_accept;
+ * SIMSD_ERR_HIP also if the array's device address cannot be obtained.
+ */
+#define SIMSD_NOALLOC_SCRATCH_BYTES ((size_t)4 << 20) /* 4 MiB per device */
+simsd_status simsd_verify_accept_noalloc(const simsd_accept_desc* desc, const void* logits,
+                                         const int32_t* draft_ids, const int32_t* step_map,
+                                         const int32_t* num_ref, int32_t* target_ids,
+                                         float* confidence, float* draft_prob,
+                                         int32_t* accept_len, void* stream);
+
+/*
  * Stochastic verification (eq. 2 at temperature T > 0, Sec. 3.2; the paper's
  * experiments use T = 1, Sec. 4.1): the rule the greedy call is the T -> 0
  * limit of.  With p_theta(r) = softmax(logits[b, k_r] / T) at the

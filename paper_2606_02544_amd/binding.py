@@ -74,6 +74,8 @@ def lib() -> ctypes.CDLL:
         L.simsd_verify_accept.argtypes = [ctypes.POINTER(AcceptDesc)] + [_P] * 8 + \
             [_P, ctypes.c_size_t, _P]
         L.simsd_verify_accept.restype = ctypes.c_int
+        L.simsd_verify_accept_noalloc.argtypes = [ctypes.POINTER(AcceptDesc)] + [_P] * 9
+        L.simsd_verify_accept_noalloc.restype = ctypes.c_int
         L.simsd_verify_accept_sampled_workspace_size.argtypes = [ctypes.POINTER(AcceptDesc)]
         L.simsd_verify_accept_sampled_workspace_size.restype = ctypes.c_size_t
         L.simsd_verify_accept_sampled.argtypes = [ctypes.POINTER(AcceptDesc), ctypes.c_float] + \
@@ -367,6 +369,38 @@ def verify_accept(logits, draft_ids, step_map, num_ref, *, chunks_per_row: int =
         ctypes.byref(desc), _ptr(logits), _ptr(draft_ids), _ptr(step_map), _ptr(num_ref),
         _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
         _ptr(workspace), _nbytes(workspace), ctypes.c_void_p(st.cuda_stream)))
+    return target_ids, confidence, draft_prob, accept_len
+
+
+NOALLOC_SCRATCH_BYTES = 4 << 20      # SIMSD_NOALLOC_SCRATCH_BYTES
+
+
+def verify_accept_noalloc(logits, draft_ids, step_map, num_ref, *, target_ids=None,
+                          confidence=None, draft_prob=None, accept_len=None, stream=None):
+    """simsd_verify_accept_noalloc on torch tensors: the greedy accept with the
+    library's fixed per-device scratch instead of a workspace (for callers that
+    cannot allocate; pass preallocated outputs to allocate nothing at all).
+    Calls overlapping on one GPU race on that scratch.
+    Returns (target_ids, confidence, draft_prob, accept_len)."""
+    b, B, V, L, dev = _check_accept_inputs(logits, draft_ids, step_map, num_ref)
+    _out("target_ids", target_ids, (b, B), torch.int32, dev)
+    _out("confidence", confidence, (b, B), torch.float32, dev)
+    _out("draft_prob", draft_prob, (b, L), torch.float32, dev)
+    _out("accept_len", accept_len, (b,), torch.int32, dev)
+    desc = accept_desc(logits, L)
+    if target_ids is None:
+        target_ids = torch.empty((b, B), dtype=torch.int32, device=dev)
+    if confidence is None:
+        confidence = torch.empty((b, B), dtype=torch.float32, device=dev)
+    if draft_prob is None:
+        draft_prob = torch.empty((b, L), dtype=torch.float32, device=dev)
+    if accept_len is None:
+        accept_len = torch.empty((b,), dtype=torch.int32, device=dev)
+    st = _stream_of(stream, dev)
+    _check(lib().simsd_verify_accept_noalloc(
+        ctypes.byref(desc), _ptr(logits), _ptr(draft_ids), _ptr(step_map), _ptr(num_ref),
+        _ptr(target_ids), _ptr(confidence), _ptr(draft_prob), _ptr(accept_len),
+        ctypes.c_void_p(st.cuda_stream)))
     return target_ids, confidence, draft_prob, accept_len
 
 

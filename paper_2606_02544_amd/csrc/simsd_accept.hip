@@ -16,7 +16,18 @@
 // the same scan over the verification rows and the drafter's rows, then the
 // acceptance test and the residual draw of the first rejection (see the
 // section further down).
+#include <atomic>
+#include <mutex>
+#include <string>
+
 #include "simsd_kernels.h"
+
+// Scratch of simsd_verify_accept_noalloc: the scan partials of one call, in a
+// fixed device array instead of a caller workspace.  Every GPU the library
+// runs on holds its own copy until the process ends.  In host code the name
+// `scratch` is only a host-side stand-in: host code uses the device address
+// that scratch_address() obtains for each device, never the name itself.
+static __device__ __align__(256) unsigned char scratch[SIMSD_NOALLOC_SCRATCH_BYTES];
 
 namespace simsd {
 namespace {
@@ -743,4 +754,100 @@ hipError_t launch_accept_sampled(const simsd_accept_desc& d, const AcceptPlan& p
   return hipGetLastError();
 }
 
+// ----------------------------------------------------------------------------
+// Allocation-free greedy accept.  The device address of `scratch` is looked up
+// once per device (with that device current) and kept; calls then pass it to
+// the same kernels simsd_verify_accept launches, in place of the workspace.
+// ----------------------------------------------------------------------------
+namespace {
+
+constexpr int kScratchDevices = 64;
+std::atomic<void*> g_scratch_ptr[kScratchDevices];
+std::mutex g_scratch_mu;
+
+hipError_t scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      int cur = 0;
+      hipError_t e = hipGetDevice(&cur);
+      if (e != hipSuccess) return e;
+      if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (cur != dev) {
+        const hipError_t e2 = hipSetDevice(cur);
+        if (e == hipSuccess) e = e2;
+      }
+      if (e != hipSuccess) return e;
+      if (!p) return hipErrorInvalidSymbol;
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return hipSuccess;
+}
+
+}  // namespace
 }  // namespace simsd
+
+extern "C" simsd_status simsd_verify_accept_noalloc(const simsd_accept_desc* desc,
+                                                    const void* logits, const int32_t* draft_ids,
+                                                    const int32_t* step_map,
+                                                    const int32_t* num_ref, int32_t* target_ids,
+                                                    float* confidence, float* draft_prob,
+                                                    int32_t* accept_len, void* stream) {
+  using namespace simsd;
+  try {
+    int dev = 0, cus = 0;
+    const hipError_t qe = stream_device(stream, &dev, &cus);
+    AcceptPlan p;
+    simsd_status st = plan_accept(desc, cus, &p);
+    if (st != SIMSD_OK) return st;
+    if (p.workspace > SIMSD_NOALLOC_SCRATCH_BYTES) {
+      set_error("accept_noalloc: this shape needs " + std::to_string(p.workspace) +
+                " bytes of scratch, more than the fixed " +
+                std::to_string(SIMSD_NOALLOC_SCRATCH_BYTES) +
+                "; call simsd_verify_accept with a workspace instead");
+      return SIMSD_ERR_WORKSPACE;
+    }
+    st = check_accept_inputs(desc, logits, draft_ids, step_map, num_ref, target_ids, accept_len);
+    if (st != SIMSD_OK) return st;
+    void* part = nullptr;
+    hipError_t e = qe;
+    if (e == hipSuccess) e = scratch_address(dev, &part);
+    if (e != hipSuccess) {
+      set_error(std::string("simsd_verify_accept_noalloc: device scratch: ") + hipGetErrorString(e));
+      return SIMSD_ERR_HIP;
+    }
+    AcceptArgs a{};
+    a.logits = logits;
+    a.draft_ids = draft_ids;
+    a.step_map = step_map;
+    a.num_ref = num_ref;
+    a.target_ids = target_ids;
+    a.confidence = confidence;
+    a.draft_prob = draft_prob;
+    a.accept_len = accept_len;
+    a.part = static_cast<AcceptPartial*>(part);
+    a.nvec = p.nvec;
+    a.chunk_vecs = p.chunk_vecs;
+    a.B = desc->block_size;
+    a.L = desc->max_ref;
+    a.V = desc->vocab;
+    a.cpr = p.cpr;
+    a.rows = p.rows;
+    a.cl = kLog2e;
+    e = launch_accept(*desc, p, a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+      set_error(std::string("simsd_verify_accept_noalloc launch: ") + hipGetErrorString(e));
+      return SIMSD_ERR_HIP;
+    }
+    return SIMSD_OK;
+  } catch (...) {
+    set_error("simsd_verify_accept_noalloc: internal error");
+    return SIMSD_ERR_HIP;
+  }
+}

@@ -40,18 +40,24 @@ static hipError_t device_cus(int dev, int* cus) {
   return hipSuccess;
 }
 
-// Compute units of the device a stream belongs to (the current device for
-// the null stream).  When the query fails, *cus is the nominal count of an
-// MI355X, so that argument errors are still reported first; the caller
-// returns the query's error after validation.
+// Device and compute units of the device a stream belongs to (the current
+// device for the null stream).  When the query fails, *cus is the nominal
+// count of an MI355X, so that argument errors are still reported first; the
+// caller returns the query's error after validation.
 static constexpr int kNominalCUs = 256;
 
-static hipError_t stream_cus(void* stream, int* cus) {
-  hipDevice_t dev = 0;
-  hipError_t e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &dev);
-  if (e == hipSuccess) e = device_cus(dev, cus);
+hipError_t simsd::stream_device(void* stream, int* dev, int* cus) {
+  hipDevice_t d = 0;
+  hipError_t e = hipStreamGetDevice(static_cast<hipStream_t>(stream), &d);
+  if (e == hipSuccess) e = device_cus(d, cus);
   if (e != hipSuccess) *cus = kNominalCUs;
+  *dev = d;
   return e;
+}
+
+static hipError_t stream_cus(void* stream, int* cus) {
+  int dev = 0;
+  return stream_device(stream, &dev, cus);
 }
 
 // Compute units of the current device (workspace-size queries have no

@@ -84,6 +84,10 @@ hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t stream);
 hipError_t launch_lmhead_merge(const LmheadArgs& a, hipStream_t st);
 hipError_t launch_finalize_lmhead(int batch, const AcceptArgs& a, hipStream_t stream);
 int lmhead_vocab_tile(int rows);   // vocabulary entries per scan work-group, by row count
+// Device of `stream` (a hipStream_t; NULL = the current device) and its
+// compute units, queried once per device; on failure *cus is an MI355X's 256
+// and the error is returned for the caller to report after validation.
+hipError_t stream_device(void* stream, int* dev, int* cus);
 int lmhead_stage();        // reduction elements per stage (H must be a multiple)
 
 }  // namespace simsd

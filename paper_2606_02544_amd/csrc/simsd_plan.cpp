@@ -226,6 +226,19 @@ simsd_status plan_accept(const simsd_accept_desc* d, int cus, AcceptPlan* p, boo
   return SIMSD_OK;
 }
 
+simsd_status check_accept_inputs(const simsd_accept_desc* d, const void* logits,
+                                 const int32_t* draft_ids, const int32_t* step_map,
+                                 const int32_t* num_ref, const int32_t* target_ids,
+                                 const int32_t* accept_len) {
+  if (!logits || !step_map || !num_ref || !target_ids || !accept_len)
+    return fail(SIMSD_ERR_NULL_POINTER,
+                "accept: logits, step_map, num_ref, target_ids and accept_len are required");
+  if (d->max_ref > 0 && !draft_ids)
+    return fail(SIMSD_ERR_NULL_POINTER, "accept: draft_ids required when max_ref > 0");
+  if (!aligned16(logits)) return fail(SIMSD_ERR_ALIGNMENT, "accept: logits must be 16-byte aligned");
+  return SIMSD_OK;
+}
+
 simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const void* logits, const int32_t* draft_ids,
                                const int32_t* step_map, const int32_t* num_ref,
@@ -234,12 +247,9 @@ simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const void* workspace, size_t workspace_bytes) {
   (void)confidence;
   (void)draft_prob;
-  if (!logits || !step_map || !num_ref || !target_ids || !accept_len)
-    return fail(SIMSD_ERR_NULL_POINTER,
-                "accept: logits, step_map, num_ref, target_ids and accept_len are required");
-  if (d->max_ref > 0 && !draft_ids)
-    return fail(SIMSD_ERR_NULL_POINTER, "accept: draft_ids required when max_ref > 0");
-  if (!aligned16(logits)) return fail(SIMSD_ERR_ALIGNMENT, "accept: logits must be 16-byte aligned");
+  const simsd_status st = check_accept_inputs(d, logits, draft_ids, step_map, num_ref,
+                                              target_ids, accept_len);
+  if (st != SIMSD_OK) return st;
   if (!workspace) return fail(SIMSD_ERR_WORKSPACE, "accept: workspace is NULL");
   if (!aligned16(workspace)) return fail(SIMSD_ERR_ALIGNMENT, "accept: workspace must be 16-byte aligned");
   if (workspace_bytes < p.workspace)

@@ -97,6 +97,11 @@ simsd_status check_attention_args(const simsd_attn_desc* d, const AttnPlan& p, c
 
 // sampled: the stochastic entry point, whose scan also covers the L draft rows.
 simsd_status plan_accept(const simsd_accept_desc* d, int cus, AcceptPlan* p, bool sampled = false);
+// The accept arguments other than the workspace.
+simsd_status check_accept_inputs(const simsd_accept_desc* d, const void* logits,
+                                 const int32_t* draft_ids, const int32_t* step_map,
+                                 const int32_t* num_ref, const int32_t* target_ids,
+                                 const int32_t* accept_len);
 simsd_status check_accept_args(const simsd_accept_desc* d, const AcceptPlan& p,
                                const void* logits, const int32_t* draft_ids,
                                const int32_t* step_map, const int32_t* num_ref,

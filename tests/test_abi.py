@@ -284,3 +284,39 @@ def test_status_strings():
     lib = binding.lib()
     for code, name in binding.STATUS.items():
         assert lib.simsd_status_string(code).decode() == name
+
+
+def call_accept_noalloc(desc, **over):
+    _no_gpu()
+    a = dict(logits=FAKE, draft_ids=FAKE, step_map=FAKE, num_ref=FAKE, target_ids=FAKE,
+             confidence=None, draft_prob=None, accept_len=FAKE)
+    a.update(over)
+    lib = binding.lib()
+    st = lib.simsd_verify_accept_noalloc(ctypes.byref(desc), a["logits"], a["draft_ids"],
+                                         a["step_map"], a["num_ref"], a["target_ids"],
+                                         a["confidence"], a["draft_prob"], a["accept_len"], None)
+    return st, lib.simsd_last_error().decode()
+
+
+def test_accept_noalloc_errors():
+    """The allocation-free accept: argument errors as simsd_verify_accept, a
+    shape whose partials exceed the fixed scratch is refused, and with no
+    device visible a valid call reports the HIP error after validation."""
+    good = dict(batch=2, block_size=4, max_ref=4, vocab=1000, chunks_per_row=0,
+                logits_dtype=binding.SIMSD_BF16)
+    for k, v, st in [("batch", 0, 2), ("block_size", 65, 2), ("vocab", 0, 2),
+                     ("logits_dtype", 3, 3)]:
+        assert call_accept_noalloc(AcceptDesc(**dict(good, **{k: v})))[0] == st, k
+    d = AcceptDesc(**good)
+    assert call_accept_noalloc(d, logits=None)[0] == 1
+    assert call_accept_noalloc(d, draft_ids=None)[0] == 1
+    assert call_accept_noalloc(d, logits=ctypes.c_void_p(0x10004))[0] == 4
+    # 65535 x 64 rows of 16-byte partials: 64 MiB, beyond the 4 MiB scratch
+    big = AcceptDesc(**dict(good, batch=65535, block_size=64, max_ref=64))
+    st, msg = call_accept_noalloc(big)
+    assert st == 5 and "scratch" in msg, msg
+    # largest shape that fits: partials of 262144 rows of one chunk each
+    fits = AcceptDesc(**dict(good, batch=4096, block_size=64, max_ref=64, vocab=151936))
+    assert binding.accept_workspace_size(fits) <= binding.NOALLOC_SCRATCH_BYTES
+    st, msg = call_accept_noalloc(fits)
+    assert st == 7 and "device" in msg, msg
