@@ -361,13 +361,15 @@ struct KVRing {
 };
 
 // RW row waves of 32 rows each; KW = 2 pairs every row wave with a second wave
-// that takes the other 32-key half of each tile (row blocks of up to 128 rows,
-// where the extra waves double the work in flight); the two halves merge at
-// the end.
+// that takes the other 32-key half of each tile (the stream decomposition and
+// row blocks of up to 64 rows, where the extra waves double the work in
+// flight); the two halves merge at the end.
 // The ring holds NBUF tiles: tile it + NBUF - 1 loads while tile it is read.
 // 8-wave groups have a CU to themselves (their registers allow no second
-// group) and keep three tiles in flight; 4-wave groups run two to a CU, each
-// with a two-tile ring (measured faster than one group with a deeper ring).
+// group) and keep three tiles in flight; 4-wave groups keep a two-tile ring
+// (measured faster than a deeper one: 3 or 4 tiles cost 13-17 % on the
+// SDAR-8B layer with four whole-tile row waves, 10-35 % with two groups per
+// CU).
 template <int D, int RW, int KW, bool PAGED, bool ROPE>
 __device__ __attribute__((always_inline)) void attend_segment(const AttnArgs& a, const Work& w) {
   constexpr int NW = RW * KW;
@@ -1094,7 +1096,7 @@ void launch_bf16_variant(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStr
   }
   switch (p.row_waves) {
     case 2: hipLaunchKernelGGL((attn_bf16_kernel<D, 2, 2, PAGED, ROPE>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED, ROPE>), grid, dim3(512), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED, ROPE>), grid, dim3(256), 0, st, a); break;
     default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED, ROPE>), grid, dim3(512), 0, st, a); break;
   }
 }

@@ -86,13 +86,16 @@ simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p) {
   r.n_new = d->block_size + d->max_ref;
   r.rows = r.group * r.n_new;
   if (d->dtype == SIMSD_BF16) {
-    // One 32-row MFMA block per row wave; a power of two in [2, 8].  With two
-    // or four row waves, each is paired with a second wave taking the other
-    // half of every key tile (4 or 8 waves per group).
+    // One 32-row MFMA block per row wave; a power of two in [2, 8].  Two row
+    // waves are each paired with a second wave taking the other half of
+    // every key tile (4 waves per group, two groups per CU); four or eight
+    // row waves take whole tiles (one group per CU).  (Four row waves with
+    // half tiles, 8 waves, measured 7-9 % slower on the SDAR-8B layer: one
+    // 32-key block per wave between barriers.)
     const int need = static_cast<int>(ceil_div(std::min(r.rows, 256), 32));
     r.row_waves = 2;
     while (r.row_waves < need) r.row_waves *= 2;
-    r.waves = r.row_waves <= 4 ? 2 * r.row_waves : r.row_waves;
+    r.waves = r.row_waves <= 2 ? 2 * r.row_waves : r.row_waves;
     r.rows_pb = r.row_waves * 32;
   } else {
     r.waves = 4;          // 8 rows per wave, one wave per row at a time
@@ -107,8 +110,8 @@ simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p) {
     r.chunk = d->kv_chunk;
   } else {
     // Split the longest prefix so that about as many work-groups exist as the
-    // chip holds at once: one 8-wave group or two smaller groups per CU.
-    const int64_t target = r.waves >= 8 ? cus : 2 * int64_t{cus};
+    // chip holds at once: one group per CU, two for the two-row-wave groups.
+    const int64_t target = r.row_waves >= 4 ? cus : 2 * int64_t{cus};
     int64_t c = ceil_div(static_cast<int64_t>(d->max_prefix_len) * r.pairs, target);
     c = ceil_div(c, kTile) * kTile;
     if (c < kMinAutoChunk) c = kMinAutoChunk;
@@ -133,7 +136,8 @@ simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p) {
                 "attention: kv_chunk -1 (stream) needs bf16, at most 128 packed rows "
                 "(Hq/Hkv * (B + L)) and batch <= 256");
   if (can_stream && d->kv_chunk <= 0) {
-    const int64_t groups = r.waves >= 8 ? cus : 2 * int64_t{cus};
+    // Stream groups: 8 waves (one per CU) for four row waves, else 4 (two per CU).
+    const int64_t groups = r.row_waves >= 4 ? cus : 2 * int64_t{cus};
     const int64_t tiles = r.pairs * (ceil_div(d->max_prefix_len, kTile) + 1);
     if (d->kv_chunk == kStreamChunk || (tiles >= 8 * groups && r.pairs * r.splits > groups)) {
       r.stream = true;
