@@ -19,6 +19,8 @@ ROPE_CASES = [
     ("bf16", 64, 8, 2, 16, 16, (0, 3000), 0, -1, 1e4, 3),      # stream decomposition
     ("bf16", 128, 12, 3, 24, 8, (0, 2500), 32, -1, 1e6, 4),    # stream, paged
     ("bf16", 128, 32, 8, 32, 32, (30000, 32800), 0, 0, 1e6, 5),  # positions past 32768
+    ("bf16", 128, 8, 2, 16, 16, (100, 700), 16, 64, 1e6, 8),   # 128 rows: 4 whole-tile row waves, paged
+    ("bf16", 64, 16, 4, 16, 16, (0, 500), 0, 0, 1e4, 9),       # 128 rows, contiguous, d 64
     ("f32", 64, 4, 2, 8, 6, (0, 200), 0, 64, 1e4, 6),
     ("f32", 128, 8, 2, 4, 4, (1, 90), 5, 0, 1e6, 7),
 ]
