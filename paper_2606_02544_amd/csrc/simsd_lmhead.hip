@@ -13,13 +13,15 @@
 // (one wave per row) and finalize_kernel (simsd_accept.hip) finds the accepted
 // prefix from them as for stored logits.
 //
-// Tiles: TR rows x TV vocabulary entries per 8-wave work-group; wave w covers
-// rows (TR/2)*(w/4).. and vocabulary (TV/4)*(w%4).. in 32 x 32 MFMA blocks.  The
-// reduction dimension streams in KS-wide stages through a ring of NBUF LDS
-// stages filled by direct global-to-LDS loads, so several stages are in
-// flight without staging registers.  A stage row holds CPR 16-byte chunks;
-// chunk c of row r sits at position c ^ swz(r), so the operand reads of 16
-// consecutive rows touch 64 distinct banks.
+// Tiles: TR rows x TV vocabulary entries per work-group of WV x WR waves (4 x 2
+// in every variant); wave w covers rows (TR/WR)*(w/WV).. and vocabulary
+// (TV/WV)*(w%WV).. in 32 x 32 MFMA blocks.  The reduction dimension streams in
+// KS-wide stages through a ring of NBUF LDS stages filled by direct
+// global-to-LDS loads, so several stages are in flight without staging
+// registers.  A stage row holds CPR 16-byte chunks; chunk c of row r sits at
+// position c ^ swz(r), so the operand reads of 16 consecutive rows touch 64
+// distinct banks.  Each wave reads the operands of the next 16-wide sub-step
+// (across the stage barrier too) while the MFMAs of the current one run.
 #include "simsd_kernels.h"
 
 namespace simsd {
@@ -31,7 +33,7 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kNoIndex = 0x7fffffff;
-constexpr int NT = 512;                  // 8 waves: 4 vocabulary quarters x 2 row halves
+constexpr int NT = 512;                  // threads of the merge kernel
 // Row-count thresholds of the variants (see launch_lmhead_scan).
 constexpr int kFewRows = 32;
 constexpr int kOneTileRows = 128;
@@ -41,6 +43,12 @@ constexpr int kOneTileRows = 128;
 // 16 bytes per lane from a per-lane address into LDS at m0 + 16 * lane.
 __device__ inline void dma16(const void* src, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+// The same with the non-temporal hint: the line is streamed through the L2
+// rather than kept there.
+__device__ inline void dma16_nt(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt"
                :: "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
 template <int N>
@@ -67,11 +75,13 @@ __device__ inline Best combine(Best a, Best b) {
 }
 
 // TR rows and TV vocabulary entries per tile, KS reduction elements per
-// stage, NBUF stages in the ring.
-template <int TR, int TV, int KS, int NBUF>
-__global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
-  constexpr int RBW = TR / 64;             // 32-row MFMA blocks per wave
-  constexpr int VBW = TV / 128;            // 32-entry MFMA blocks per wave
+// stage, NBUF stages in the ring; WV x WR waves (vocabulary parts x row parts).
+// STREAMW: the weight is loaded with the non-temporal hint.
+template <int TR, int TV, int KS, int NBUF, int WV, int WR, bool STREAMW>
+__global__ void __launch_bounds__(64 * WV * WR) lmhead_scan_kernel(LmheadArgs a) {
+  constexpr int NT = 64 * WV * WR;
+  constexpr int RBW = TR / (32 * WR);      // 32-row MFMA blocks per wave
+  constexpr int VBW = TV / (32 * WV);      // 32-entry MFMA blocks per wave
   constexpr int CPR = KS / 8;              // 16-byte chunks per row per stage
   constexpr int ROWB = KS * 2;             // LDS bytes per row per stage
   constexpr int RPS = 16 / CPR;            // rows spanning the 64 banks
@@ -79,17 +89,17 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   constexpr int INSN = STAGEB / 1024;      // 1 KB direct loads per stage
   constexpr int PERW = INSN / (NT / 64);   // per wave
   constexpr int RPI = 64 / CPR;            // rows per direct load
-  static_assert(RBW >= 1 && TR % 64 == 0 && VBW >= 1 && TV % 128 == 0, "wave grid");
+  static_assert(RBW >= 1 && TR % (32 * WR) == 0 && VBW >= 1 && TV % (32 * WV) == 0, "wave grid");
   static_assert(KS % 16 == 0 && CPR <= 16, "stage width");
   static_assert(INSN % (NT / 64) == 0, "stage loads split evenly over the waves");
   static_assert(NBUF >= 2 && NBUF <= 5, "ring depth");
   auto swz = [](int r) { return (r / RPS) % CPR; };
   __shared__ __attribute__((aligned(1024))) uint8_t s_ring[NBUF][STAGEB];
-  __shared__ Best s_part[4][TR];          // per vocabulary quarter, per row of the tile
+  __shared__ Best s_part[WV][TR];         // per vocabulary part, per row of the tile
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, h = lane >> 5;
-  const int rw = wave / 4, vq = wave % 4;
+  const int rw = wave / WV, vq = wave % WV;
   // Work-groups go to the eight XCDs round-robin.  Tile t = xcd * per + j
   // (row tiles fastest) keeps the row tiles of one vocabulary tile on one XCD,
   // whose L2 then serves them the weight tile once; ids past the last tile
@@ -124,7 +134,10 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     const int64_t off = static_cast<int64_t>(s) * KS * 2;
     const uint32_t slot = ring0 + (s % NBUF) * STAGEB;
 #pragma unroll
-    for (int i = 0; i < PERW; ++i) dma16(src[i] + off, slot + dst[i]);
+    for (int i = 0; i < PERW; ++i) {
+      if (STREAMW && RPI * (wave * PERW + i) < TV) dma16_nt(src[i] + off, slot + dst[i]);
+      else dma16(src[i] + off, slot + dst[i]);
+    }
   };
 
   f32x16 acc[VBW][RBW];                    // [vocab block][row block]
@@ -142,12 +155,12 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   for (int ks = 0; ks < KSUB; ++ks) {
 #pragma unroll
     for (int vb = 0; vb < VBW; ++vb) {
-      const int rv = (TV / 4) * vq + 32 * vb + n;
+      const int rv = (TV / WV) * vq + 32 * vb + n;
       ao[ks][vb] = rv * ROWB + 16 * ((2 * ks + h) ^ swz(rv));
     }
 #pragma unroll
     for (int rb = 0; rb < RBW; ++rb) {
-      const int rr = TV + (TR / 2) * rw + 32 * rb + n;
+      const int rr = TV + (TR / WR) * rw + 32 * rb + n;
       bo[ks][rb] = rr * ROWB + 16 * ((2 * ks + h) ^ swz(rr));
     }
   }
@@ -156,7 +169,9 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
 #pragma unroll
   for (int s = 0; s < NBUF - 1; ++s)
     if (s < S) issue(s);
-  for (int s = 0; s < S; ++s) {
+  // Stage s is waited for, and the ring slot of stage s - 1 refilled, once
+  // every wave has passed the barrier.
+  auto enter_stage = [&](int s) __attribute__((always_inline)) {
     // Stages issued: 0 .. min(S, s + NBUF - 1) - 1; stage s has landed once
     // at most the younger ones remain.
     const int younger = min(S, s + NBUF - 1) - 1 - s;
@@ -166,27 +181,58 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     else wait_vm<0>();
     lds_barrier();                         // stage s is in; stage s - 1's slot is free
     if (s + NBUF - 1 < S) issue(s + NBUF - 1);
-    const LM_LDS uint8_t* st = reinterpret_cast<const LM_LDS uint8_t*>(ring0) + (s % NBUF) * STAGEB;
+  };
+  auto stage_at = [&](int s) __attribute__((always_inline)) {
+    return reinterpret_cast<const LM_LDS uint8_t*>(ring0) + (s % NBUF) * STAGEB;
+  };
+  // Operand fragments in two register sets: the reads of sub-step ks + 1 (or
+  // of the next stage's first sub-step) are in flight while the MFMAs of
+  // sub-step ks run.
+  static_assert(KSUB % 2 == 0, "sub-steps alternate between two fragment sets");
+  bf16x8 fa[2][VBW], fb[2][RBW];
+  auto read_frags = [&](const LM_LDS uint8_t* st, int ks, int set) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ks = 0; ks < KSUB; ++ks) {
-      bf16x8 fa[VBW], fb[RBW];
+    for (int vb = 0; vb < VBW; ++vb) fa[set][vb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + ao[ks][vb]);
 #pragma unroll
-      for (int vb = 0; vb < VBW; ++vb) fa[vb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + ao[ks][vb]);
+    for (int rb = 0; rb < RBW; ++rb) fb[set][rb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + bo[ks][rb]);
+  };
+  auto mfmas = [&](int set) __attribute__((always_inline)) {
 #pragma unroll
-      for (int rb = 0; rb < RBW; ++rb) fb[rb] = *reinterpret_cast<const LM_LDS bf16x8*>(st + bo[ks][rb]);
+    for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
-      for (int vb = 0; vb < VBW; ++vb)
+      for (int rb = 0; rb < RBW; ++rb)
+        acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[set][vb], fb[set][rb], acc[vb][rb], 0, 0, 0);
+  };
+  if (S > 0) {
+    enter_stage(0);
+    read_frags(stage_at(0), 0, 0);
+  }
+  for (int s = 0; s < S; ++s) {
+    const LM_LDS uint8_t* st = stage_at(s);
 #pragma unroll
-        for (int rb = 0; rb < RBW; ++rb)
-          acc[vb][rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[vb], fb[rb], acc[vb][rb], 0, 0, 0);
+    for (int ks = 0; ks < KSUB - 1; ++ks) {
+      read_frags(st, ks + 1, (ks + 1) & 1);
+      mfmas(ks & 1);
     }
+    // The last sub-step's fragments are in registers, so the barrier that
+    // enters the next stage may pass before its MFMAs issue.
+    if (s + 1 < S) {
+      enter_stage(s + 1);
+      read_frags(stage_at(s + 1), 0, 0);
+    }
+    mfmas(1);
   }
 
   // Epilogue.  Register j of acc[vb][rb] holds vocabulary entry
-  // v0 + (TV/4)*vq + 32*vb + 8*(j/4) + 4*h + j%4 of row r0 + (TR/2)*rw + 32*rb + n.
+  // v0 + (TV/WV)*vq + 32*vb + 8*(j/4) + 4*h + j%4 of row r0 + (TR/WR)*rw + 32*rb + n.
 #pragma unroll
   for (int rb = 0; rb < RBW; ++rb) {
-    const int rowl = (TR / 2) * rw + 32 * rb + n, row = r0 + rowl;
+    const int rowl = (TR / WR) * rw + 32 * rb + n, row = r0 + rowl;
+    float xv[VBW][16];
+#pragma unroll
+    for (int vb = 0; vb < VBW; ++vb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) xv[vb][j] = acc[vb][rb][j];
     // The drafted token of this row, if it is a verification row.
     int tok = -1, slot = -1;
     if (row < a.R) {
@@ -204,8 +250,8 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
     for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
-        const int v = v0 + (TV / 4) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
-        const float x = acc[vb][rb][j];
+        const int v = v0 + (TV / WV) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
+        const float x = xv[vb][j];
         if (v < a.V) {
           if (x > mx || (x == mx && v < ix)) {
             mx = x;
@@ -220,8 +266,8 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
       for (int vb = 0; vb < VBW; ++vb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int v = v0 + (TV / 4) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
-          if (v < a.V) sm += __builtin_amdgcn_exp2f((acc[vb][rb][j] - mx) * kLog2e);
+          const int v = v0 + (TV / WV) * vq + 32 * vb + 8 * (j >> 2) + 4 * h + (j & 3);
+          if (v < a.V) sm += __builtin_amdgcn_exp2f((xv[vb][j] - mx) * kLog2e);
         }
     }
     Best me = {mx, ix, sm};
@@ -236,7 +282,7 @@ __global__ void __launch_bounds__(NT) lmhead_scan_kernel(LmheadArgs a) {
   if (tid < TR && r0 + tid < a.R) {
     Best r = s_part[0][tid];
 #pragma unroll
-    for (int q = 1; q < 4; ++q) r = combine(r, s_part[q][tid]);
+    for (int q = 1; q < WV; ++q) r = combine(r, s_part[q][tid]);
     AcceptPartial pr;
     pr.mx = r.mx;
     pr.ix = r.ix;
@@ -299,12 +345,12 @@ __global__ void __launch_bounds__(NT) lmhead_merge_kernel(LmheadArgs a) {
 }  // namespace
 
 namespace {
-template <int TR, int TV, int KS, int NBUF>
+template <int TR, int TV, int KS, int NBUF, int WV = 4, int WR = 2, bool STREAMW = false>
 hipError_t launch_variant(const LmheadArgs& a, hipStream_t st) {
   if (a.vtiles != (a.V + TV - 1) / TV) return hipErrorInvalidValue;   // plan and launch disagree
   const int ntiles = (a.R + TR - 1) / TR * a.vtiles;
-  hipLaunchKernelGGL((lmhead_scan_kernel<TR, TV, KS, NBUF>), dim3((ntiles + 7) / 8 * 8), dim3(NT),
-                     0, st, a);
+  hipLaunchKernelGGL((lmhead_scan_kernel<TR, TV, KS, NBUF, WV, WR, STREAMW>), dim3((ntiles + 7) / 8 * 8),
+                     dim3(64 * WV * WR), 0, st, a);
   return hipGetLastError();
 }
 }  // namespace
@@ -312,10 +358,13 @@ hipError_t launch_variant(const LmheadArgs& a, hipStream_t st) {
 hipError_t launch_lmhead_scan(const LmheadArgs& a, hipStream_t st) {
   // Few rows: the weight stream is all there is; 128-entry vocabulary tiles
   // (more, shorter work-groups) and 54 KB of LDS, two work-groups per CU.  Up
-  // to one row tile: 128-byte row segments, one work-group per CU.  More rows:
-  // 256-row tiles halve the weight re-reads and the LDS reads per MFMA.
+  // to one row tile: 128-byte row segments, one work-group per CU, and the
+  // weight (read by no other work-group) streamed past the L2 so that the
+  // L2 keeps the hidden rows every work-group re-reads.  More rows: 256-row
+  // tiles halve the weight re-reads and the LDS reads per MFMA; the two row
+  // tiles of a vocabulary tile share its weight lines through the L2.
   if (a.R <= kFewRows) return launch_variant<128, 128, 32, 3>(a, st);
-  if (a.R <= kOneTileRows) return launch_variant<128, 256, 64, 3>(a, st);
+  if (a.R <= kOneTileRows) return launch_variant<128, 256, 64, 3, 4, 2, true>(a, st);
   return launch_variant<256, 256, 64, 2>(a, st);
 }
 
