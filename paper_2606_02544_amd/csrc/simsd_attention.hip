@@ -958,9 +958,12 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 }
 
 // ----------------------------------------------------------------------------
-// Merge of split partials.  Grid: (32-row groups of a row block, KV head x row
-// block, sequence); one thread per (row, 4 dims).  Sequences whose prefix fits
-// one chunk were finished by the attention kernel and are skipped.
+// Merge of split partials.  Grid: (thread blocks over the packed rows of a row
+// block, KV head x row block, sequence); one thread per (row, DPT dims of the
+// output): 16 bytes of each partial, 8 dims of a bf16 partial or 4 of an fp32
+// one, or 4 bf16 dims where many splits make each thread's loads long.
+// Sequences whose prefix fits one chunk were finished by the attention kernel
+// and are skipped.
 // ----------------------------------------------------------------------------
 // Merge of the partials of each pair.  Chunked decomposition: the pair's
 // nsplit chunk partials.  Stream decomposition: the partials of the groups
@@ -969,9 +972,10 @@ __global__ void __launch_bounds__(256) attn_f32_kernel(AttnArgs a) {
 // range was written whole by that group.
 // SB partials are loaded per round (indices clamped, so a round always loads
 // SB); the launcher takes SB near the split count.
-template <int D, typename OutT, bool STREAM, int SB>
+template <int D, typename OutT, bool STREAM, int SB, int DPT = 16 / static_cast<int>(sizeof(OutT))>
 __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
-  constexpr int D4 = D / 4;
+  static_assert(DPT == 4 || (DPT == 8 && sizeof(OutT) == 2), "dims per thread");
+  constexpr int TPR = D / DPT;                                // threads per row
   // A zero the compiler cannot see through: keeps the per-sequence reads
   // vector loads issued with the others instead of late scalar loads.
   int lane_zero;
@@ -979,7 +983,7 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   const int b = blockIdx.z;
   const int kvh = blockIdx.y / a.row_blocks, rb = blockIdx.y % a.row_blocks;
   const int idx = blockIdx.x * 256 + threadIdx.x;
-  const int rowl = idx / D4, d0 = (idx % D4) * 4;
+  const int rowl = idx / TPR, d0 = (idx % TPR) * DPT;
   // Rows past the packed rows of this block have no partials.
   if (rowl >= a.rows_pb || rb * a.rows_pb + rowl >= a.rows) return;
   const int rl = rowl;
@@ -1023,19 +1027,31 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     }
   };
   float mv[SB], lv[SB];
-  f32x4 ov[SB];
+  float ov[SB][DPT];
   auto load_round = [&](int s0) {
 #pragma unroll
     for (int s = 0; s < SB; ++s) {
       const float* ps = part_of(s0 + s);
       mv[s] = ps[mo + rl];
       lv[s] = ps[mo + a.rows_pb + rl];
-      if constexpr (sizeof(OutT) == 2) {       // bf16 partials, normalised by their sum
+      if constexpr (sizeof(OutT) == 2 && DPT == 8) {   // bf16 partials, normalised by their sum
+        const u32x4 w4 = *reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(ps) + rl * D + d0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          ov[s][2 * e] = __uint_as_float(w4[e] << 16);
+          ov[s][2 * e + 1] = __uint_as_float(w4[e] & 0xffff0000u);
+        }
+      } else if constexpr (sizeof(OutT) == 2) {
         const u32x2 w2 = *reinterpret_cast<const u32x2*>(reinterpret_cast<const uint16_t*>(ps) + rl * D + d0);
-        ov[s] = f32x4{__uint_as_float(w2[0] << 16), __uint_as_float(w2[0] & 0xffff0000u),
-                      __uint_as_float(w2[1] << 16), __uint_as_float(w2[1] & 0xffff0000u)};
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          ov[s][2 * e] = __uint_as_float(w2[e] << 16);
+          ov[s][2 * e + 1] = __uint_as_float(w2[e] & 0xffff0000u);
+        }
       } else {
-        ov[s] = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
+        const f32x4 f4 = *reinterpret_cast<const f32x4*>(ps + rl * D + d0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ov[s][e] = f4[e];
       }
     }
   };
@@ -1047,7 +1063,9 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   const bool valid = t < a.B ? step >= 0 : (t - a.B) < gamma;
 
   float mt = kNegInf, lsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  float acc[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) acc[e] = 0.f;
   for (int s0 = 0; s0 < nsplit; s0 += SB) {
     if (s0 > 0) load_round(s0);
     float mb = kNegInf;
@@ -1058,14 +1076,17 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
     if (mn == kNegInf) continue;
     const float alpha = __builtin_amdgcn_exp2f(mt - mn);   // 0 while mt is -inf
     lsum *= alpha;
-    acc *= alpha;
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) acc[e] *= alpha;
 #pragma unroll
     for (int s = 0; s < SB; ++s) {
       if (s0 + s < nsplit) {
         const float wt = __builtin_amdgcn_exp2f(mv[s] - mn);
         lsum += wt * lv[s];
         // bf16 partials hold O / l: their weight carries the sum.
-        acc += (sizeof(OutT) == 2 ? wt * lv[s] : wt) * ov[s];
+        const float wo = sizeof(OutT) == 2 ? wt * lv[s] : wt;
+#pragma unroll
+        for (int e = 0; e < DPT; ++e) acc[e] += wo * ov[s][e];
       }
     }
     mt = mn;
@@ -1073,11 +1094,16 @@ __global__ void __launch_bounds__(256) merge_kernel(AttnArgs a) {
   const bool ok = valid && lsum > 0.f;
   const float inv = ok ? 1.f / lsum : 0.f;
   const int64_t orow = ((static_cast<int64_t>(b) * a.n_new + t) * a.hq + hq) * D + d0;
-  if constexpr (sizeof(OutT) == 2) {
+  if constexpr (sizeof(OutT) == 2 && DPT == 8) {
+    const u32x4 pk = {pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv),
+                      pack2(acc[4] * inv, acc[5] * inv), pack2(acc[6] * inv, acc[7] * inv)};
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.out) + orow) = pk;
+  } else if constexpr (sizeof(OutT) == 2) {
     const u32x2 pk = {pack2(acc[0] * inv, acc[1] * inv), pack2(acc[2] * inv, acc[3] * inv)};
     *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.out) + orow) = pk;
   } else {
-    *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) = acc * inv;
+    *reinterpret_cast<f32x4*>(static_cast<float*>(a.out) + orow) =
+        f32x4{acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv};
   }
   if (d0 == 0 && a.lse)
     a.lse[(static_cast<int64_t>(b) * a.hq + hq) * a.n_new + t] =
@@ -1109,13 +1135,19 @@ void launch_bf16(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStream_t st
   else launch_bf16_variant<D, PAGED, false>(p, grid, a, st);
 }
 
-// Chunked merge: loads per round near the split count.
+// Chunked merge: loads per round near the split count; above 8 splits each
+// thread takes 4 dims (twice the threads, half the registers per load round).
 template <int D, typename OutT>
 void launch_merge(int splits, dim3 grid, const AttnArgs& a, hipStream_t st) {
   if (splits <= 2) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 2>), grid, dim3(256), 0, st, a);
   else if (splits <= 4) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 4>), grid, dim3(256), 0, st, a);
   else if (splits <= 8) hipLaunchKernelGGL((merge_kernel<D, OutT, false, 8>), grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((merge_kernel<D, OutT, false, 16>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((merge_kernel<D, OutT, false, 16, 4>), grid, dim3(256), 0, st, a);
+}
+
+// Dims per merge thread (see merge_kernel).
+inline int merge_dims(const AttnPlan& p, bool bf16) {
+  return bf16 && (p.stream || p.splits <= 8) ? 8 : 4;
 }
 
 template <int D>
@@ -1144,13 +1176,16 @@ hipError_t launch_attention(const simsd_attn_desc& d, const AttnPlan& p, const A
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || (p.splits <= 1 && !p.stream)) return e;
-  // Threads for the packed rows only (the last row block may be partial).
-  const int per_block = (std::min(p.rows_pb, p.rows) * d.head_dim / 4 + 255) / 256;
-  const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
+  // Threads for the packed rows only (the last row block may be partial), one
+  // per merge_dims() dims of a row.
   const bool bf16 = d.dtype == SIMSD_BF16;
+  const int per_block = (std::min(p.rows_pb, p.rows) * d.head_dim / merge_dims(p, bf16) + 255) / 256;
+  const dim3 mgrid(per_block, d.num_kv_heads * p.row_blocks, d.batch);
   if (p.stream) {
-    if (d.head_dim == 128) hipLaunchKernelGGL((merge_kernel<128, uint16_t, true, 8>), mgrid, dim3(256), 0, st, a);
-    else hipLaunchKernelGGL((merge_kernel<64, uint16_t, true, 8>), mgrid, dim3(256), 0, st, a);
+    // A pair meets a few group ranges (two or three on the ragged batches);
+    // more take further rounds.
+    if (d.head_dim == 128) hipLaunchKernelGGL((merge_kernel<128, uint16_t, true, 4>), mgrid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((merge_kernel<64, uint16_t, true, 4>), mgrid, dim3(256), 0, st, a);
   } else if (d.head_dim == 128) {
     if (bf16) launch_merge<128, uint16_t>(p.splits, mgrid, a, st);
     else launch_merge<128, float>(p.splits, mgrid, a, st);
