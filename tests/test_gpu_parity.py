@@ -143,10 +143,12 @@ MIXED = [
     ("bf16", 64, 16, 2, 8, 8, (0, 500), 8, -1, 20),        # stream, 128 rows, d 64, 8-token pages
     ("bf16", 128, 16, 2, 4, 4, (0, 700), 64, 0, 21),       # pages of exactly one tile
     ("bf16", 64, 4, 4, 8, 8, (0, 400), 4, 64, 22),         # 4-token pages (one page per 4 rows)
+    ("bf16", 128, 8, 2, 8, 8, (600, 1100), 0, 64, 23),     # 10-18 splits: 4-dim merge, two rounds
     ("f32", 64, 2, 1, 4, 4, (0, 100), 0, 64, 9),
     ("f32", 128, 8, 2, 6, 4, (1, 90), 5, 64, 10),
     ("f32", 128, 4, 1, 8, 8, (0, 0), 0, 0, 11),
     ("f32", 64, 16, 2, 16, 16, (30, 150), 0, 0, 12),
+    ("f32", 128, 4, 2, 4, 4, (500, 1100), 16, 64, 24),     # up to 18 splits, paged
 ]
 
 
