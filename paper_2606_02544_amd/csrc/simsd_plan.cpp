@@ -91,7 +91,8 @@ simsd_status plan_attention(const simsd_attn_desc* d, int cus, AttnPlan* p) {
     // every key tile (4 waves per group, two groups per CU); four or eight
     // row waves take whole tiles (one group per CU).  (Four row waves with
     // half tiles, 8 waves, measured 7-9 % slower on the SDAR-8B layer: one
-    // 32-key block per wave between barriers.)
+    // 32-key block per wave between barriers.  The rotary variant keeps them:
+    // the whole-tile one needs more registers than its bound allows.)
     const int need = static_cast<int>(ceil_div(std::min(r.rows, 256), 32));
     r.row_waves = 2;
     while (r.row_waves < need) r.row_waves *= 2;
