@@ -1127,7 +1127,7 @@ void launch_bf16_variant(const AttnPlan& p, dim3 grid, const AttnArgs& a, hipStr
       // than two groups per CU allow; it spilled the tile loads' lane offsets,
       // and each reload's wait drained the ring (SDAR-8B layer with RoPE 70.5
       // against 45.3 us for the 8-wave half-tile groups).
-      if (ROPE) hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED, ROPE>), grid, dim3(512), 0, st, a);
+      if constexpr (ROPE) hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 2, PAGED, ROPE>), grid, dim3(512), 0, st, a);
       else hipLaunchKernelGGL((attn_bf16_kernel<D, 4, 1, PAGED, ROPE>), grid, dim3(256), 0, st, a);
       break;
     default: hipLaunchKernelGGL((attn_bf16_kernel<D, 8, 1, PAGED, ROPE>), grid, dim3(512), 0, st, a); break;
