@@ -571,9 +571,8 @@ def main():
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: --gpus {args.gpus} is not supported "
-              "(this build runs on a single GPU; the verification step would shard by "
-              "sequence / KV head with no exchange, as the design notes describe).",
-              file=sys.stderr)
+              "(the verification step would shard by sequence or KV head, with no "
+              "exchange between GPUs).", file=sys.stderr)
         sys.exit(2)
 
     import torch
