@@ -1,7 +1,8 @@
 """GPU: the allocation-free accept entry point (simsd_verify_accept_noalloc)
 through the C ABI against simsd_verify_accept with a workspace, on two calls in
 a row (the second with a smaller input) and on a second stream: the outputs are
-the same bits, and both match the oracle."""
+the same bits, and both match the oracle.  Also captured in a HIP graph, with
+eager calls on other inputs between the replays."""
 
 import ctypes
 
@@ -66,6 +67,42 @@ def test_noalloc_matches_workspace_entry_point():
     d = DeviceInputs(big)
     s = torch.cuda.Stream()
     _same(_noalloc(d, s), _with_workspace(d))
+
+
+def test_noalloc_in_a_captured_graph():
+    """The allocation-free accept captured in a HIP graph (its callers include
+    code under graph capture): every replay reproduces the eager outputs bit
+    for bit, also after eager calls on another input have overwritten the
+    shared scratch in between."""
+    from paper_2606_02544_amd import binding
+    a = DeviceInputs(generate(CONFIGS[3].replace(batch=2, prefix=64), seed=21))
+    other = DeviceInputs(generate(VerifyConfig(0, "other", "bf16", batch=4, num_q_heads=2,
+                                               num_kv_heads=1, head_dim=64, prefix=8,
+                                               block_size=8, max_ref=8, vocab=5003,
+                                               step_mode="mixed"), seed=22))
+    eager = binding.verify_accept_noalloc(a.logits, a.draft_ids, a.step_map, a.num_ref)
+    torch.cuda.synchronize()
+    outs = [torch.zeros_like(t) for t in eager]
+    kw = dict(target_ids=outs[0], confidence=outs[1], draft_prob=outs[2], accept_len=outs[3])
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        binding.verify_accept_noalloc(a.logits, a.draft_ids, a.step_map, a.num_ref, stream=s, **kw)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            binding.verify_accept_noalloc(a.logits, a.draft_ids, a.step_map, a.num_ref,
+                                          stream=s, **kw)
+    for rep in range(4):
+        for t in outs:
+            t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _same(outs, eager)
+        # eager work on another input between replays, through the same scratch
+        binding.verify_accept_noalloc(other.logits, other.draft_ids, other.step_map,
+                                      other.num_ref)
+        torch.cuda.synchronize()
 
 
 def test_noalloc_refuses_oversized_shapes():
